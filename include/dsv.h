@@ -1,0 +1,210 @@
+/*
+ * dsv.h -- C ABI of the block-diffusion speculative-decoding verify path
+ * (DScale, "Scaling Block-Diffusion Speculative Decoding with Adaptive
+ * Verification"), built for AMD Instinct MI355X (gfx950).
+ *
+ * The library exposes the two operations of the target-verification hot path:
+ *
+ *   dsv_verify_attn  ragged, packed verify attention over a paged bf16 GQA KV
+ *                    cache (Sec. III-B tile routing, Sec. III-D Eq. (16) row
+ *                    validity, and the packed layout of Eqs. (10)-(11));
+ *   dsv_accept       greedy acceptance: per-row vocabulary argmax followed by
+ *                    the longest-prefix compare against the drafted tokens
+ *                    (Sec. III-D "Prefix verifier", greedy case; Sec. I
+ *                    definition of accepted tokens).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every data pointer is a DEVICE pointer owned by the caller.  The library
+ *    keeps no pointer after the call returns and allocates nothing.
+ *  - Calls only enqueue work on `hip_stream` (a hipStream_t; NULL = the null
+ *    stream).  They never synchronise, never read device memory from the
+ *    host and never allocate, so they may be recorded into a hipGraph.  The
+ *    caller keeps every buffer alive until the enqueued work has finished.
+ *  - Host-known arguments are validated before anything is enqueued; on a
+ *    validation failure nothing is enqueued and a negative dsv_status is
+ *    returned.  The library never aborts the process.
+ *  - Device-resident metadata (cu_qlens, ctx_lens, page_table, draft_tokens)
+ *    cannot be validated on the host without a synchronisation.  The kernels
+ *    re-check it cheaply: a request whose metadata breaks a precondition
+ *    below is skipped (its outputs are left untouched), a page id outside
+ *    [0, num_pages) is never dereferenced, and no access leaves the buffers
+ *    described here.  dsv_validate_metadata reports such violations.
+ *  - Notation: B = num_reqs, G = num_q_heads / num_kv_heads (GQA group),
+ *    D = head_dim, k_i = cu_qlens[i+1] - cu_qlens[i] = verify length of
+ *    request i (1 anchor + k_i - 1 drafted candidates; 0 for a sentinel
+ *    request that occupies no rows), W = 16 = block width (anchor + 15).
+ */
+#ifndef DSV_H
+#define DSV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DSV_OK = 0,
+  DSV_ERR_NULL = -1,        /* a required pointer is NULL                      */
+  DSV_ERR_DIMS = -2,        /* a host-known size is out of range               */
+  DSV_ERR_UNSUPPORTED = -3, /* valid but unsupported (head_dim, page size, G)  */
+  DSV_ERR_WORKSPACE = -4,   /* workspace NULL, misaligned or too small         */
+  DSV_ERR_HIP = -5          /* a HIP runtime call failed (launch error)        */
+} dsv_status;
+
+typedef enum { DSV_F32 = 0, DSV_BF16 = 1 } dsv_dtype;
+
+/* Largest verify length per request: one anchor plus 15 candidates (Sec. II). */
+#define DSV_MAX_QLEN 16
+/* Tokens per KV page.  The paper cites paged attention without fixing a page
+ * size; the library supports exactly 16. */
+#define DSV_PAGE_SIZE 16
+
+/*
+ * Dimensions of one verify_attn call.  All fields are host values.
+ *
+ *  num_reqs          B >= 1, the request bucket N_bs (Eq. (14)); requests with
+ *                    k_i = 0 are sentinels (Alg. 1's tail requests).
+ *  capacity          packed row capacity M_bs of q_packed / out (Eq. (3)),
+ *                    >= 1.  Rows cu_qlens[B] .. capacity-1 are tail rows.
+ *  num_q_heads       Hq >= 1.
+ *  num_kv_heads      Hkv >= 1, Hq % Hkv == 0, G = Hq / Hkv in {1,2,4,8,16}.
+ *  head_dim          D in {64, 128}.
+ *  page_size         must be DSV_PAGE_SIZE (16).
+ *  max_pages_per_req P_max >= 1, the row stride of page_table.
+ *  num_pages         pages in kv_pages; page ids must lie in [0, num_pages).
+ *  max_kv_len        an upper bound on ctx_lens[i] + k_i over every call that
+ *                    uses the same workspace (it sizes the split partials),
+ *                    1 <= max_kv_len <= P_max * 16.
+ *  scale             softmax scale applied to q.k (normally 1/sqrt(D)).
+ */
+typedef struct {
+  int32_t num_reqs;
+  int32_t capacity;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t page_size;
+  int32_t max_pages_per_req;
+  int32_t num_pages;
+  int32_t max_kv_len;
+  float scale;
+} dsv_attn_dims;
+
+/*
+ * Workspace bytes dsv_verify_attn needs for `dims` (0 if dims are invalid).
+ * The workspace holds the fp32 split-KV partials; it needs no initialisation
+ * and its contents after a call are unspecified.  Its address may stay fixed
+ * across steps (Eq. (13)), so a captured graph can be replayed.
+ */
+size_t dsv_verify_attn_workspace_bytes(const dsv_attn_dims *dims);
+
+/*
+ * Ragged packed verify attention (Eq. (16); Eqs. (10)-(11) packing).
+ *
+ * For every request i with k_i > 0, every query head h (KV head g = h / G:
+ * consecutive query heads share a KV head), and every row j < k_i:
+ *
+ *   out[cu_qlens[i]+j][h][:] = softmax_t( scale * q . K_t ) . V_t
+ *
+ * over the keys t = 0 .. ctx_lens[i] + j, i.e. the whole committed context
+ * plus the request's own block up to and including row j (request-local
+ * causal masking).  K_t / V_t are read from logical position t of request i:
+ * page page_table[i*P_max + t/16], slot t%16.  The block's own K/V (anchor and
+ * candidates, the paper's "KV refs") must already sit at positions
+ * ctx_lens[i] .. ctx_lens[i]+k_i-1 of the same page table.  Tail rows
+ * (cu_qlens[B] .. capacity-1) of `out` are written with zeros.  Positional
+ * encoding is already applied to q and K.
+ *
+ * Layouts (bf16 = IEEE binary32 truncated to its upper 16 bits, stored as
+ * uint16; all arrays dense, row-major, no padding):
+ *   q_packed    bf16 [capacity][Hq][D]; row cu_qlens[i]+j is block row j of i.
+ *   cu_qlens    int32 [B+1], cu_qlens[0] = 0, non-decreasing,
+ *               k_i <= DSV_MAX_QLEN, cu_qlens[B] <= capacity.
+ *   kv_pages    bf16 [num_pages][2][Hkv][16*D]; [..][0][g] is the K tile and
+ *               [..][1][g] the V tile of KV head g in that page:
+ *                 K tile: element (slot s, dim d) at ((d/8)*16 + s)*8 + d%8
+ *                         (8-element d-chunks, slot-major inside a chunk);
+ *                 V tile: element (slot s, dim d) at d*16 + s (d-major).
+ *               Each tile is 16*D*2 bytes (4 KiB at D=128).
+ *   page_table  int32 [B][P_max]; only the first ceil((ctx_i+k_i)/16) entries
+ *               of row i are read.
+ *   ctx_lens    int32 [B], committed context EXCLUDING the verify block, >= 0,
+ *               ctx_i + k_i <= max_kv_len.
+ *   out         bf16 [capacity][Hq][D], written (every row).
+ *   workspace   >= dsv_verify_attn_workspace_bytes(dims) bytes, 256-byte
+ *               aligned.
+ * Accumulation is fp32 with one rounding to bf16 (round-to-nearest-even) at
+ * the end.  The result for a request does not depend on how the other
+ * requests are packed.
+ */
+int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
+                    const void *kv_pages, const int32_t *page_table,
+                    const int32_t *ctx_lens, void *out,
+                    const dsv_attn_dims *dims, void *workspace,
+                    size_t workspace_bytes, void *hip_stream);
+
+/*
+ * Workspace bytes dsv_accept needs (0 if the sizes are invalid).  It holds
+ * per-(row, vocabulary chunk) maxima; it needs no initialisation.
+ */
+size_t dsv_accept_workspace_bytes(int32_t capacity, int32_t num_reqs,
+                                  int32_t vocab);
+
+/*
+ * Greedy acceptance (Sec. III-D "Prefix verifier" at temperature 0, where the
+ * target policy is one-hot at its argmax; Sec. I: accepted tokens are the
+ * contiguous candidate prefix that the target reproduces, anchor excluded).
+ *
+ * For every live row r < cu_qlens[B]:  t_r = argmax_v logits_packed[r][v]
+ * (exact comparison of the stored values; ties go to the lowest v).
+ * For request i with o = cu_qlens[i] and k = k_i:
+ *   k == 0:  accept_len[i] = 0, next_token[i] = -1 (sentinel request);
+ *   k >= 1:  accept_len[i] = a = the largest m <= k-1 such that
+ *            t_{o+j} == draft_tokens[o+j+1] for every j < m;
+ *            next_token[i] = t_{o+a} (the successor that anchors the next
+ *            step: the target's choice at the first rejection, or after the
+ *            last accepted candidate).
+ *
+ * Layouts:
+ *   logits_packed  [capacity][vocab] of `dtype` (DSV_F32 or DSV_BF16), dense;
+ *                  values of live rows must be finite (NaN order undefined).
+ *   cu_qlens       int32 [B+1], as for dsv_verify_attn (same buffer).
+ *   draft_tokens   int32 [capacity]: the packed verify INPUT ids -- the anchor
+ *                  at row cu_qlens[i], candidate j at row cu_qlens[i]+j.
+ *   accept_len     int32 [B], written.
+ *   next_token     int32 [B], written.
+ *   workspace      >= dsv_accept_workspace_bytes(...) bytes, 256-byte aligned.
+ * Rows at or beyond cu_qlens[B] are never read.  The result is exact.
+ */
+int dsv_accept(const void *logits_packed, int32_t dtype,
+               const int32_t *cu_qlens, const int32_t *draft_tokens,
+               int32_t *accept_len, int32_t *next_token, int32_t num_reqs,
+               int32_t capacity, int32_t vocab, void *workspace,
+               size_t workspace_bytes, void *hip_stream);
+
+/*
+ * Debug check of device metadata (the preconditions listed above).  Enqueues
+ * one small kernel that writes, into *err_word (device int32), a bit mask of
+ * the violated rules (0 = all hold):
+ *   1  cu_qlens[0] != 0 or not non-decreasing
+ *   2  some k_i > DSV_MAX_QLEN
+ *   4  cu_qlens[B] > capacity
+ *   8  some ctx_lens[i] < 0 or ctx_i + k_i > max_kv_len
+ *  16  a page id that verify_attn would read lies outside [0, num_pages)
+ * The caller reads *err_word after synchronising the stream.
+ */
+int dsv_validate_metadata(const int32_t *cu_qlens, const int32_t *ctx_lens,
+                          const int32_t *page_table, const dsv_attn_dims *dims,
+                          int32_t *err_word, void *hip_stream);
+
+/* Static text for a dsv_status value ("unknown status" otherwise). */
+const char *dsv_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DSV_H */

@@ -1,0 +1,129 @@
+"""Plain fp64 CPU oracle of the verify hot path (C, loaded with ctypes).
+
+TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  It shares no code
+with the HIP library (``paper_2609_37532_amd``) and never imports it.
+
+Functions take numpy arrays; bf16 tensors are ``uint16`` arrays holding the
+upper half of IEEE binary32 values.  See ``oracle.c`` for the definitions and
+the paper passages each one follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_HDR = os.path.join(_HERE, "oracle.h")
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile ``liboracle.so`` with gcc (strict IEEE double, no fast-math)."""
+    if not force and os.path.exists(LIB_PATH) and os.path.getmtime(LIB_PATH) >= max(
+        os.path.getmtime(_SRC), os.path.getmtime(_HDR)
+    ):
+        return LIB_PATH
+    tmp = LIB_PATH + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fno-fast-math",
+           "-ffp-contract=off", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    build(force=False)
+    lib = ctypes.CDLL(LIB_PATH)
+    p = ctypes.c_void_p
+    i32 = ctypes.c_int32
+    lib.oracle_verify_attn.argtypes = [p, p, p, p, p, p, i32, i32, i32, i32, i32,
+                                       i32, i32, i32, ctypes.c_double]
+    lib.oracle_verify_attn.restype = ctypes.c_int
+    lib.oracle_row_argmax.argtypes = [p, i32, i32, i32, p]
+    lib.oracle_row_argmax.restype = ctypes.c_int
+    lib.oracle_accept.argtypes = [p, i32, p, p, p, p, i32, i32, i32]
+    lib.oracle_accept.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def verify_attn(q, cu_qlens, kv_pages, page_table, ctx_lens, *, num_q_heads,
+                num_kv_heads, head_dim, page_size, scale, capacity=None):
+    """fp64 verify attention; returns ``out`` float64 [capacity, Hq, D].
+
+    ``q`` uint16 [cap, Hq, D]; ``kv_pages`` uint16 [P, 2, Hkv, page*D];
+    ``page_table`` int32 [B, P_max]; ``cu_qlens`` int32 [B+1];
+    ``ctx_lens`` int32 [B].
+    """
+    lib = _load()
+    q = _c(q, np.uint16)
+    kv = _c(kv_pages, np.uint16)
+    cu = _c(cu_qlens, np.int32)
+    pt = _c(page_table, np.int32)
+    ctx = _c(ctx_lens, np.int32)
+    cap = q.shape[0] if capacity is None else capacity
+    B = ctx.shape[0]
+    assert cu.shape[0] == B + 1 and pt.shape[0] == B
+    out = np.empty((cap, num_q_heads, head_dim), dtype=np.float64)
+    rc = lib.oracle_verify_attn(_ptr(q), _ptr(cu), _ptr(kv), _ptr(pt), _ptr(ctx),
+                                _ptr(out), B, cap, num_q_heads, num_kv_heads,
+                                head_dim, page_size, pt.shape[1], kv.shape[0],
+                                float(scale))
+    if rc != 0:
+        raise ValueError("oracle_verify_attn rejected its input (rc=%d)" % rc)
+    return out
+
+
+def _logits_args(logits, dtype):
+    if dtype == "f32":
+        return _c(logits, np.float32), 0
+    if dtype == "bf16":
+        return _c(logits, np.uint16), 1
+    raise ValueError(dtype)
+
+
+def row_argmax(logits, dtype):
+    """Lowest-index argmax of each row; ``dtype`` is 'f32' or 'bf16' (uint16 bits)."""
+    lib = _load()
+    lg, code = _logits_args(logits, dtype)
+    rows, vocab = lg.shape
+    idx = np.empty(rows, dtype=np.int32)
+    rc = lib.oracle_row_argmax(_ptr(lg), code, rows, vocab, _ptr(idx))
+    if rc != 0:
+        raise ValueError("oracle_row_argmax rejected its input (rc=%d)" % rc)
+    return idx
+
+
+def accept(logits, dtype, cu_qlens, draft_tokens):
+    """Greedy acceptance; returns ``(accept_len, next_token)`` int32 [B]."""
+    lib = _load()
+    lg, code = _logits_args(logits, dtype)
+    cu = _c(cu_qlens, np.int32)
+    dr = _c(draft_tokens, np.int32)
+    cap, vocab = lg.shape
+    B = cu.shape[0] - 1
+    a = np.empty(B, dtype=np.int32)
+    nxt = np.empty(B, dtype=np.int32)
+    rc = lib.oracle_accept(_ptr(lg), code, _ptr(cu), _ptr(dr), _ptr(a), _ptr(nxt),
+                           B, cap, vocab)
+    if rc != 0:
+        raise ValueError("oracle_accept rejected its input (rc=%d)" % rc)
+    return a, nxt

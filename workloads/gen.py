@@ -1,0 +1,408 @@
+"""Seeded synthetic workloads shaped like the paper's verify step.
+
+The paper evaluates Qwen3-8B / Qwen3-4B targets with a W = 16 block (one
+anchor + 15 DFlash candidates, Sec. II) at concurrency 8-32 (Sec. IV-A).
+Weights, drafters and datasets are not used: every tensor here is drawn from
+a seeded ``numpy.random.Generator`` (PCG64), with the shapes of those models'
+attention layers (32 query / 8 KV heads, head_dim 128, vocabulary 151,936)
+and length distributions from a geometric acceptance model.
+
+Draw order inside one preset (fixed, so a seed pins every byte):
+  1. verify lengths (if sampled), 2. context lengths (if sampled),
+  3. physical page permutation, 4. q values, 5. KV pool values,
+  6. acceptance: draft tokens, planted accept lengths, rejection tokens,
+     logit noise.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Optional, Sequence
+
+import numpy as np
+
+SEED_BASE = 20260901
+BF16_NAN = np.uint16(0x7FC0)
+PAGE_SIZE = 16
+BLOCK_WIDTH = 16  # W: anchor + 15 candidates
+
+
+# --------------------------------------------------------------------------
+# bf16 storage helpers (format conversion of inputs, not method arithmetic)
+# --------------------------------------------------------------------------
+def bf16_bits(x) -> np.ndarray:
+    """float32 -> bf16 bit patterns (uint16), round to nearest even."""
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    u = f.view(np.uint32)
+    rounding = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + rounding) >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_to_f32(bits) -> np.ndarray:
+    b = np.ascontiguousarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _normal_bf16(rng: np.random.Generator, shape, scale: float = 1.0,
+                 chunk: int = 1 << 24) -> np.ndarray:
+    """N(0, scale^2) draws stored as bf16, generated in chunks to bound memory."""
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint16)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        x = rng.standard_normal(e - s, dtype=np.float32)
+        if scale != 1.0:
+            x *= np.float32(scale)
+        out[s:e] = bf16_bits(x)
+    return out.reshape(shape)
+
+
+# --------------------------------------------------------------------------
+# KV page layout of the library contract (where slot s, dim c of a tile lives)
+# --------------------------------------------------------------------------
+def k_tile_offset(slot, dim, page_size: int = PAGE_SIZE):
+    """Element offset of (slot, dim) inside a K tile: 8-wide dim chunks."""
+    slot = np.asarray(slot)
+    dim = np.asarray(dim)
+    return ((dim // 8) * page_size + slot) * 8 + dim % 8
+
+
+def v_tile_offset(slot, dim, page_size: int = PAGE_SIZE):
+    """Element offset of (slot, dim) inside a V tile: dim-major."""
+    slot = np.asarray(slot)
+    dim = np.asarray(dim)
+    return dim * page_size + slot
+
+
+# --------------------------------------------------------------------------
+# lengths and offsets
+# --------------------------------------------------------------------------
+def verify_lengths(rng: np.random.Generator, num_reqs: int, capacity: int,
+                   p: float = 0.25, width: int = BLOCK_WIDTH) -> np.ndarray:
+    """Per-request verify lengths: anchor + truncated geometric prefix.
+
+    k_i = min(G_i, W) with G_i ~ Geometric(p) on {1, 2, ...}, i.e.
+    1 + min(G_i - 1, W - 1).  Only if the total exceeds ``capacity``: scale
+    proportionally (floor, at least 1), then decrement the largest (lowest
+    index first) until the total fits.
+    """
+    g = rng.geometric(p, size=num_reqs)
+    k = np.minimum(g, width).astype(np.int64)
+    total = int(k.sum())
+    if total > capacity:
+        if capacity < num_reqs:
+            raise ValueError("capacity below one row per request")
+        k = np.maximum(1, (k * capacity) // total)
+        while int(k.sum()) > capacity:
+            k[int(np.argmax(k))] -= 1
+    return k.astype(np.int32)
+
+
+def cu_from_lengths(lengths: Sequence[int]) -> np.ndarray:
+    """Packed row offsets: (0, k_0, k_0+k_1, ...) as int32 [B+1]."""
+    k = np.asarray(lengths, dtype=np.int64)
+    cu = np.zeros(k.shape[0] + 1, dtype=np.int64)
+    cu[1:] = np.cumsum(k)
+    return cu.astype(np.int32)
+
+
+# --------------------------------------------------------------------------
+# attention inputs
+# --------------------------------------------------------------------------
+@dataclass
+class AttnInputs:
+    q: np.ndarray            # uint16 [capacity, Hq, D]
+    cu_qlens: np.ndarray     # int32 [B+1]
+    kv_pages: np.ndarray     # uint16 [num_pages, 2, Hkv, page*D]
+    page_table: np.ndarray   # int32 [B, P_max]; -1 beyond a request's pages
+    ctx_lens: np.ndarray     # int32 [B]
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    page_size: int
+    max_kv_len: int
+    scale: float
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def num_reqs(self) -> int:
+        return int(self.ctx_lens.shape[0])
+
+    @property
+    def capacity(self) -> int:
+        return int(self.q.shape[0])
+
+    @property
+    def num_pages(self) -> int:
+        return int(self.kv_pages.shape[0])
+
+    @property
+    def max_pages(self) -> int:
+        return int(self.page_table.shape[1])
+
+    @property
+    def qlens(self) -> np.ndarray:
+        return np.diff(self.cu_qlens).astype(np.int32)
+
+    def dims(self) -> dict:
+        return dict(num_reqs=self.num_reqs, capacity=self.capacity,
+                    num_q_heads=self.num_q_heads, num_kv_heads=self.num_kv_heads,
+                    head_dim=self.head_dim, page_size=self.page_size,
+                    max_pages_per_req=self.max_pages, num_pages=self.num_pages,
+                    max_kv_len=self.max_kv_len, scale=self.scale)
+
+    def oracle_kwargs(self) -> dict:
+        return dict(num_q_heads=self.num_q_heads, num_kv_heads=self.num_kv_heads,
+                    head_dim=self.head_dim, page_size=self.page_size,
+                    scale=self.scale)
+
+
+def make_attn_inputs(rng: np.random.Generator, *, ctx_lens, qlens, capacity: int,
+                     num_q_heads: int, num_kv_heads: int, head_dim: int,
+                     page_size: int = PAGE_SIZE, max_kv_len: Optional[int] = None,
+                     scale: Optional[float] = None, permute_pages: bool = True,
+                     spare_pages: int = 0, poison: bool = True,
+                     q_scale: float = 1.0) -> AttnInputs:
+    """Paged attention inputs with Q, K, V ~ N(0,1) in bf16.
+
+    Request i owns ceil((ctx_i + k_i) / page) pages; physical ids are a random
+    permutation of the pool when ``permute_pages``.  With ``poison``, every
+    element that verify attention must NOT read is set to bf16 NaN: tail rows
+    of q, slots at or beyond ctx_i + k_i in a request's last page, and
+    ``spare_pages`` extra pool pages nobody references.
+    """
+    ctx = np.asarray(ctx_lens, dtype=np.int32)
+    k = np.asarray(qlens, dtype=np.int32)
+    B = ctx.shape[0]
+    assert k.shape[0] == B
+    cu = cu_from_lengths(k)
+    if int(cu[-1]) > capacity:
+        raise ValueError("packed rows exceed capacity")
+    keys = ctx.astype(np.int64) + k
+    if max_kv_len is None:
+        max_kv_len = int(max(1, keys.max()))
+    if int(keys.max()) > max_kv_len:
+        raise ValueError("ctx + k exceeds max_kv_len")
+    max_pages = -(-max_kv_len // page_size)
+    need = [(-(-int(L) // page_size)) if kk > 0 else 0 for L, kk in zip(keys, k)]
+    used = int(sum(need))
+    num_pages = max(1, used + spare_pages)
+    ids = rng.permutation(num_pages).astype(np.int32) if permute_pages else \
+        np.arange(num_pages, dtype=np.int32)
+    page_table = np.full((B, max_pages), -1, dtype=np.int32)
+    pos = 0
+    for i in range(B):
+        page_table[i, :need[i]] = ids[pos:pos + need[i]]
+        pos += need[i]
+
+    q = _normal_bf16(rng, (capacity, num_q_heads, head_dim), q_scale)
+    kv = _normal_bf16(rng, (num_pages, 2, num_kv_heads, page_size * head_dim))
+
+    if poison:
+        q[int(cu[-1]):] = BF16_NAN
+        for p in ids[used:]:
+            kv[p] = BF16_NAN
+        dims = np.arange(head_dim)
+        for i in range(B):
+            if need[i] == 0:
+                continue
+            last = page_table[i, need[i] - 1]
+            first_dead = int(keys[i]) - (need[i] - 1) * page_size
+            for s in range(first_dead, page_size):
+                kv[last, 0, :, k_tile_offset(s, dims, page_size)] = BF16_NAN
+                kv[last, 1, :, v_tile_offset(s, dims, page_size)] = BF16_NAN
+    if scale is None:
+        scale = 1.0 / float(np.sqrt(head_dim))
+    return AttnInputs(q=q, cu_qlens=cu, kv_pages=kv, page_table=page_table,
+                      ctx_lens=ctx, num_q_heads=num_q_heads,
+                      num_kv_heads=num_kv_heads, head_dim=head_dim,
+                      page_size=page_size, max_kv_len=int(max_kv_len),
+                      scale=float(scale))
+
+
+def repack(inp: AttnInputs, order: Sequence[int], capacity: Optional[int] = None,
+           gaps: Optional[Sequence[int]] = None, poison: bool = True) -> AttnInputs:
+    """The same requests packed differently (input rearrangement only).
+
+    Request ``order[n]`` of ``inp`` becomes the n-th live request; its q rows,
+    context length and page-table row move with it and the KV pool is shared
+    unchanged.  ``gaps[n]`` sentinel requests (k = 0) are inserted before it;
+    ``gaps`` may carry one extra trailing entry.  ``meta['moves']`` lists
+    (old_request, new_request, old_row, new_row, k) for the live requests.
+    """
+    order = list(order)
+    gaps = list(gaps) if gaps is not None else []
+    gaps += [0] * (len(order) + 1 - len(gaps))
+    entries = []
+    for n, i in enumerate(order):
+        entries += [None] * gaps[n]
+        entries.append(i)
+    entries += [None] * gaps[len(order)]
+    old_cu = inp.cu_qlens
+    new_k = [0 if e is None else int(old_cu[e + 1] - old_cu[e]) for e in entries]
+    cu = cu_from_lengths(new_k)
+    cap = capacity if capacity is not None else max(1, int(cu[-1]))
+    if int(cu[-1]) > cap:
+        raise ValueError("packed rows exceed capacity")
+    q = np.full((cap, inp.num_q_heads, inp.head_dim),
+                BF16_NAN if poison else 0, dtype=np.uint16)
+    page_table = np.full((len(entries), inp.max_pages), -1, dtype=np.int32)
+    ctx = np.zeros(len(entries), dtype=np.int32)
+    moves = []
+    for r, e in enumerate(entries):
+        if e is None:
+            continue
+        kk = new_k[r]
+        o_old, o_new = int(old_cu[e]), int(cu[r])
+        q[o_new:o_new + kk] = inp.q[o_old:o_old + kk]
+        page_table[r] = inp.page_table[e]
+        ctx[r] = inp.ctx_lens[e]
+        moves.append((e, r, o_old, o_new, kk))
+    out = AttnInputs(q=q, cu_qlens=cu, kv_pages=inp.kv_pages, page_table=page_table,
+                     ctx_lens=ctx, num_q_heads=inp.num_q_heads,
+                     num_kv_heads=inp.num_kv_heads, head_dim=inp.head_dim,
+                     page_size=inp.page_size, max_kv_len=inp.max_kv_len,
+                     scale=inp.scale)
+    out.meta["moves"] = moves
+    return out
+
+
+# --------------------------------------------------------------------------
+# acceptance inputs (planted scheme)
+# --------------------------------------------------------------------------
+@dataclass
+class AcceptInputs:
+    logits: np.ndarray          # float32 [cap, V] or uint16 bf16 bits [cap, V]
+    dtype: str                  # 'f32' | 'bf16'
+    cu_qlens: np.ndarray        # int32 [B+1]
+    draft_tokens: np.ndarray    # int32 [cap]
+    planted_accept_len: np.ndarray  # int32 [B]
+    planted_next: np.ndarray        # int32 [B]
+
+    @property
+    def vocab(self) -> int:
+        return int(self.logits.shape[1])
+
+    @property
+    def capacity(self) -> int:
+        return int(self.logits.shape[0])
+
+    @property
+    def num_reqs(self) -> int:
+        return int(self.cu_qlens.shape[0] - 1)
+
+
+def make_accept_inputs(rng: np.random.Generator, *, cu_qlens, capacity: int,
+                       vocab: int, dtype: str = "f32", p_accept: float = 0.3,
+                       boost: float = 10.0, poison: bool = True) -> AcceptInputs:
+    """Planted acceptance: logits ~ N(0,1); for request i (o = cu[i], k = k_i)
+    draw a_i = min(G - 1, k - 1), G ~ Geometric(p_accept); add ``boost`` to
+    the logit of draft_tokens[o+j+1] at row o+j for j < a_i, and to a token
+    x_i at row o+a_i, with x_i != draft_tokens[o+a_i+1] when a_i < k-1.  By
+    construction the greedy verifier accepts a_i candidates and emits x_i
+    (barring a noise draw that beats the boosted one).  Draft tokens are
+    uniform in [0, vocab).  Tail rows are NaN when ``poison``.
+    """
+    cu = np.asarray(cu_qlens, dtype=np.int32)
+    B = cu.shape[0] - 1
+    draft = rng.integers(0, vocab, size=capacity, dtype=np.int64).astype(np.int32)
+    a = np.zeros(B, dtype=np.int32)
+    nxt = np.full(B, -1, dtype=np.int32)
+    for i in range(B):
+        k = int(cu[i + 1] - cu[i])
+        if k == 0:
+            continue
+        g = int(rng.geometric(p_accept))
+        a[i] = min(g - 1, k - 1)
+    for i in range(B):
+        o, k = int(cu[i]), int(cu[i + 1] - cu[i])
+        if k == 0:
+            continue
+        if a[i] < k - 1:
+            avoid = int(draft[o + a[i] + 1])
+            x = (avoid + 1 + int(rng.integers(0, vocab - 1))) % vocab
+        else:
+            x = int(rng.integers(0, vocab))
+        nxt[i] = x
+    logits = np.empty((capacity, vocab), dtype=np.float32)
+    for r0 in range(0, capacity, 64):
+        r1 = min(capacity, r0 + 64)
+        logits[r0:r1] = rng.standard_normal((r1 - r0, vocab), dtype=np.float32)
+    for i in range(B):
+        o, k = int(cu[i]), int(cu[i + 1] - cu[i])
+        if k == 0:
+            continue
+        for j in range(int(a[i])):
+            logits[o + j, draft[o + j + 1]] += np.float32(boost)
+        logits[o + int(a[i]), nxt[i]] += np.float32(boost)
+    if poison:
+        logits[int(cu[-1]):] = np.nan
+    if dtype == "bf16":
+        stored = bf16_bits(logits)
+        if poison:
+            stored[int(cu[-1]):] = BF16_NAN
+    elif dtype == "f32":
+        stored = logits
+    else:
+        raise ValueError(dtype)
+    return AcceptInputs(logits=stored, dtype=dtype, cu_qlens=cu, draft_tokens=draft,
+                        planted_accept_len=a, planted_next=nxt)
+
+
+# --------------------------------------------------------------------------
+# the workload presets
+# --------------------------------------------------------------------------
+CONFIGS = {
+    1: dict(name="tiny", num_reqs=2, num_q_heads=4, num_kv_heads=1, head_dim=64,
+            capacity=32, ctx=[37, 100], qlens=[16, 5], vocab=1000,
+            accept_dtype="f32", p_accept=0.3),
+    2: dict(name="qwen3-4b-shape unpacked", num_reqs=8, num_q_heads=32,
+            num_kv_heads=8, head_dim=128, capacity=128, ctx_range=(256, 2048),
+            qlens="full"),
+    3: dict(name="qwen3-8b-shape packed", num_reqs=16, num_q_heads=32,
+            num_kv_heads=8, head_dim=128, capacity=128, ctx_range=(512, 4096),
+            qlens="geometric"),
+    4: dict(name="qwen3-8b-shape verify+accept c32", num_reqs=32, num_q_heads=32,
+            num_kv_heads=8, head_dim=128, capacity=256, ctx_range=(1024, 8192),
+            qlens="geometric", vocab=151936, accept_dtype="bf16", p_accept=0.3),
+}
+
+
+def config_rng(index: int) -> np.random.Generator:
+    return np.random.default_rng(SEED_BASE + index)
+
+
+def config_attn_inputs(index: int, rng: Optional[np.random.Generator] = None,
+                       poison: bool = True) -> AttnInputs:
+    """Attention inputs of preset ``index`` (draws 1-5 of the fixed order)."""
+    c = CONFIGS[index]
+    rng = config_rng(index) if rng is None else rng
+    B = c["num_reqs"]
+    if c.get("qlens") == "full":
+        k = np.full(B, BLOCK_WIDTH, dtype=np.int32)
+    elif c.get("qlens") == "geometric":
+        k = verify_lengths(rng, B, c["capacity"], p=0.25)
+    else:
+        k = np.asarray(c["qlens"], dtype=np.int32)
+    if "ctx_range" in c:
+        lo, hi = c["ctx_range"]
+        ctx = rng.integers(lo, hi + 1, size=B).astype(np.int32)
+        max_kv_len = hi + BLOCK_WIDTH
+    else:
+        ctx = np.asarray(c["ctx"], dtype=np.int32)
+        max_kv_len = int((ctx + k).max())
+    inp = make_attn_inputs(rng, ctx_lens=ctx, qlens=k, capacity=c["capacity"],
+                           num_q_heads=c["num_q_heads"],
+                           num_kv_heads=c["num_kv_heads"], head_dim=c["head_dim"],
+                           max_kv_len=max_kv_len, poison=poison)
+    inp.meta["config"] = index
+    inp.meta["name"] = c["name"]
+    return inp
+
+
+def config_accept_inputs(index: int, cu_qlens, rng: np.random.Generator,
+                         poison: bool = True) -> AcceptInputs:
+    """Acceptance inputs of preset ``index`` (draw 6), after its attention draws."""
+    c = CONFIGS[index]
+    return make_accept_inputs(rng, cu_qlens=cu_qlens, capacity=c["capacity"],
+                              vocab=c["vocab"], dtype=c["accept_dtype"],
+                              p_accept=c["p_accept"], poison=poison)
