@@ -1,0 +1,272 @@
+"""Benchmark of the verify hot path on one MI355X.
+
+One step = one replay of a captured hipGraph holding the whole path on one
+batch: verify attention (split kernel + combine kernel) for one attention
+layer, then greedy acceptance (argmax kernel + prefix kernel).  Workload:
+Qwen3-8B attention shape at concurrency 32 -- B=32 requests, 32 query / 8 KV
+heads, head_dim 128, bf16 paged KV (page 16), contexts uniform in
+[1024, 8192], verify lengths 1..16 (anchor + truncated geometric, p=0.25)
+packed into capacity 256, acceptance over bf16 logits [256 x 151936] with
+the planted geometric accept lengths.  Inputs are synthetic and seeded, and
+resident in HBM before the timed region.
+
+Prints one JSON line.  ``value`` = packed verify tokens per second of the
+whole step (sum of live verify lengths / step time).  ``roofline`` is for
+the dominant kernel (the attention split kernel), timed with HIP events on
+its stream; ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "packed verify tokens/s + HBM GB/s (% peak) per layer, Qwen3-8B shape, B=8/16/32"
+UNIT = "packed verify tokens/s"
+HBM_PEAK_GBPS = 8000.0
+CONFIG_INDEX = 4
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "attn_split_config4_counters.json")
+ATTN_SOURCE = os.path.join(ROOT, "paper_2609_37532_amd", "csrc", "attn.hip")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+def attention_bytes(attn, hkv, hq, d):
+    """Algorithmic HBM bytes of one verify-attention launch: every live key's
+    K and V once per KV head, q read and out written once per live row, plus
+    the metadata (offsets, context lengths, the page-table entries used)."""
+    k = attn.qlens.astype(np.int64)
+    keys = attn.ctx_lens.astype(np.int64) + k
+    live = k > 0
+    kv = int((keys[live] * hkv * d * 2 * 2).sum())
+    qo = int(k.sum()) * hq * d * 2 * 2
+    pages = int(((keys[live] + 15) // 16).sum())
+    meta = (attn.num_reqs + 1 + attn.num_reqs + pages) * 4
+    return kv + qo + meta
+
+
+def accept_bytes(acc, esize):
+    """Algorithmic bytes of acceptance: live logit rows once, the draft
+    tokens of live rows, offsets, and the two outputs."""
+    live = int(acc.cu_qlens[-1])
+    return live * acc.vocab * esize + live * 4 + (acc.num_reqs + 1) * 4 + 2 * acc.num_reqs * 4
+
+
+def attention_flops(attn, hq, d):
+    """q.k and p.v flops over the visible keys of every live row."""
+    tot = 0
+    for ctx, k in zip(attn.ctx_lens.astype(np.int64), attn.qlens.astype(np.int64)):
+        vis = k * ctx + k * (k + 1) // 2  # sum_j (ctx + j + 1)
+        tot += int(vis) * hq * 4 * d
+    return tot
+
+
+def counters_traffic(nbytes_alg):
+    """HBM traffic from committed rocprofv3 counter runs, if they were taken
+    on the current attention source; else None."""
+    try:
+        with open(COUNTERS_FILE) as f:
+            c = json.load(f)
+        src = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()
+        if c.get("attn_source_sha256") != src:
+            return None
+        return int(c["hbm_bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def cpu_baseline(attn, acc, seconds):
+    """fp64 oracle on the first requests of the batch (attention rows of the
+    request + its acceptance rows), until ``seconds`` of CPU time are spent."""
+    import oracle
+    import workloads as W
+    done_tokens, done_reqs, t_total = 0, 0, 0.0
+    for i in range(attn.num_reqs):
+        k = int(attn.qlens[i])
+        if k == 0:
+            continue
+        sub = W.repack(attn, [i], capacity=k)
+        o = int(attn.cu_qlens[i])
+        sub_logits = acc.logits[o:o + k]
+        sub_draft = acc.draft_tokens[o:o + k]
+        t0 = time.perf_counter()
+        oracle.verify_attn(sub.q, sub.cu_qlens, sub.kv_pages, sub.page_table,
+                           sub.ctx_lens, **sub.oracle_kwargs())
+        oracle.accept(sub_logits, acc.dtype, np.array([0, k], np.int32), sub_draft)
+        t_total += time.perf_counter() - t0
+        done_tokens += k
+        done_reqs += 1
+        if t_total >= seconds:
+            break
+    return {"value": done_tokens / t_total, "unit": UNIT, "cores": 1, "kind": "oracle",
+            "sample": "first %d of %d requests of the same batch (%d packed rows): fp64 "
+                      "attention over their keys + acceptance of their rows, %.1f s, "
+                      "single thread" % (done_reqs, attn.num_reqs, done_tokens, t_total)}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(requested --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), flush=True)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_37532_amd as dsv
+    import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda", 0)
+    t0 = time.time()
+    rng = W.config_rng(CONFIG_INDEX)
+    attn = W.config_attn_inputs(CONFIG_INDEX, rng=rng)
+    acc = W.config_accept_inputs(CONFIG_INDEX, attn.cu_qlens, rng)
+    log("inputs generated in %.1f s: B=%d, sum k=%d, %d pages"
+        % (time.time() - t0, attn.num_reqs, int(attn.qlens.sum()), attn.num_pages))
+
+    def bf16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(
+            torch.bfloat16)
+
+    def i32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+    q, kv = bf16(attn.q), bf16(attn.kv_pages)
+    cu, pt, ctx = i32(attn.cu_qlens), i32(attn.page_table), i32(attn.ctx_lens)
+    out = torch.zeros_like(q)
+    logits = bf16(acc.logits)
+    draft = i32(acc.draft_tokens)
+    a_len = torch.zeros(attn.num_reqs, dtype=torch.int32, device=dev)
+    nxt = torch.zeros_like(a_len)
+    dims = dsv.attn_dims(q, kv, pt, max_kv_len=attn.max_kv_len, scale=attn.scale)
+    ws_attn = dsv.alloc_workspace(dsv.verify_attn_workspace_bytes(dims), dev)
+    ws_acc = dsv.alloc_workspace(
+        dsv.accept_workspace_bytes(acc.capacity, acc.num_reqs, acc.vocab), dev)
+    stream = torch.cuda.Stream(device=dev)
+
+    def step_on(s):
+        dsv.verify_attn(q, cu, kv, pt, ctx, out, dims=dims, workspace=ws_attn, stream=s)
+        dsv.accept(logits, cu, draft, a_len, nxt, workspace=ws_acc, stream=s)
+
+    torch.cuda.synchronize()
+    step_on(stream)  # eager run once before capture
+    torch.cuda.synchronize()
+    graph = dsv.Graph().capture(lambda: step_on(stream), stream)
+    log("graph captured")
+
+    # ---- timed region: K graph replays of the whole step
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            graph.replay(stream)
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(args.steps):
+            graph.replay(stream)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    tokens = int(attn.qlens.sum())
+    value = tokens / (ms_step / 1e3)
+    log("step %.1f us, %.0f tokens/s" % (ms_step * 1e3, value))
+
+    # ---- kernel durations: HIP events around each kernel on its stream
+    n_timed = max(args.steps, 20)
+    for _ in range(3):
+        step_on(stream)
+    torch.cuda.synchronize()
+    timer = dsv.KernelTimer(max_launches=4 * n_timed + 16)
+    with timer:
+        for _ in range(n_timed):
+            step_on(stream)
+        torch.cuda.synchronize()
+    t_split = timer.mean_ms("attn_split") * 1e-3
+    t_comb = timer.mean_ms("attn_combine") * 1e-3
+    t_argmax = timer.mean_ms("accept_argmax") * 1e-3
+    t_prefix = timer.mean_ms("accept_prefix") * 1e-3
+
+    hq, hkv, d = attn.num_q_heads, attn.num_kv_heads, attn.head_dim
+    b_attn = attention_bytes(attn, hkv, hq, d)
+    b_acc = accept_bytes(acc, 2)
+    f_attn = attention_flops(attn, hq, d)
+    achieved = b_attn / t_split / 1e9
+    traffic = counters_traffic(b_attn)
+    a_gbps = b_acc / t_argmax / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; Qwen3-8B attention shapes, no weights)",
+        "config": {
+            "workload": "verify attention (1 layer) + greedy acceptance, Qwen3-8B shape, "
+                        "B=32, 32q/8kv heads, head_dim 128, page 16, ctx U[1024,8192], "
+                        "verify lengths 1..16 (geometric p=0.25) packed in capacity 256, "
+                        "bf16 logits [256 x 151936]",
+            "global_batch": attn.num_reqs,
+            "packed_tokens": tokens,
+            "kv_tokens": int((attn.ctx_lens + attn.qlens).sum()),
+            "capacity": attn.capacity,
+            "step": "one hipGraph replay: attn split + combine + argmax + prefix",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "attn_split_kernel<128>",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes": b_attn,
+            "launch_us": round(t_split * 1e6, 2),
+        },
+        "us_per_layer_attention": round((t_split + t_comb) * 1e6, 2),
+        "attention_gbps": round(b_attn / (t_split + t_comb) / 1e9, 1),
+        "attention_tflops": round(f_attn / (t_split + t_comb) / 1e12, 2),
+        "accept": {"argmax_us": round(t_argmax * 1e6, 2), "prefix_us": round(t_prefix * 1e6, 2),
+                   "algorithmic_bytes": b_acc, "argmax_gbps": round(a_gbps, 1),
+                   "argmax_frac": round(a_gbps / HBM_PEAK_GBPS, 4)},
+        "combine_us": round(t_comb * 1e6, 2),
+    }
+    graph.close()
+
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        result["cpu_baseline"] = cpu_baseline(attn, acc, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -136,9 +136,12 @@ size_t dsv_verify_attn_workspace_bytes(const dsv_attn_dims *dims);
  *   out         bf16 [capacity][Hq][D], written (every row).
  *   workspace   >= dsv_verify_attn_workspace_bytes(dims) bytes, 256-byte
  *               aligned.
- * Accumulation is fp32 with one rounding to bf16 (round-to-nearest-even) at
- * the end.  The result for a request does not depend on how the other
- * requests are packed.
+ * Precision: q.k products, the softmax and all accumulation are fp32; the
+ * softmax weights enter the weighted sum of V rounded to bf16 (and the same
+ * rounded weights form the normaliser); `out` is rounded once to bf16
+ * (round-to-nearest-even).  The result for a request is deterministic and
+ * does not depend on how the other requests are packed or on which physical
+ * pages hold its keys.
  */
 int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
                     const void *kv_pages, const int32_t *page_table,
@@ -199,6 +202,42 @@ int dsv_accept(const void *logits_packed, int32_t dtype,
 int dsv_validate_metadata(const int32_t *cu_qlens, const int32_t *ctx_lens,
                           const int32_t *page_table, const dsv_attn_dims *dims,
                           int32_t *err_word, void *hip_stream);
+
+/*
+ * Graph helpers for the fixed-address replay of Alg. 2 (capture once, replay
+ * each step) under the workspace invariant of Eq. (13): while a stream is
+ * being captured, dsv_verify_attn / dsv_accept calls (and any other work
+ * enqueued on it) are recorded instead of run; the instantiated graph then
+ * replays them with the same buffer addresses, whose CONTENTS (lengths,
+ * offsets, page tables, q, logits) may change between replays.
+ *
+ *  dsv_graph_capture_begin  starts capture on `hip_stream` (must not be the
+ *                           null stream; thread-local capture mode).
+ *  dsv_graph_capture_end    ends capture and instantiates; *graph_exec
+ *                           receives an opaque handle owned by the caller
+ *                           (NULL on failure).
+ *  dsv_graph_replay         enqueues one replay on `hip_stream`.
+ *  dsv_graph_destroy        releases the handle.
+ * All return a dsv_status.
+ */
+int dsv_graph_capture_begin(void *hip_stream);
+int dsv_graph_capture_end(void *hip_stream, void **graph_exec);
+int dsv_graph_replay(void *graph_exec, void *hip_stream);
+int dsv_graph_destroy(void *graph_exec);
+
+/*
+ * Kernel timing for measurement harnesses.  After dsv_timing_start(n), the
+ * next n kernel launches made by eager (not captured) dsv_verify_attn /
+ * dsv_accept calls are bracketed by HIP events recorded on the caller's
+ * stream.  dsv_timing_stop waits for those events, writes per kernel kind the
+ * summed milliseconds and the launch count (arrays of DSV_TIMING_KINDS), and
+ * turns timing off.  Kinds: 0 attention split kernel, 1 attention combine
+ * kernel, 2 vocabulary argmax kernel, 3 prefix-compare kernel.  Not
+ * thread-safe against concurrent calls from several host threads.
+ */
+#define DSV_TIMING_KINDS 4
+int dsv_timing_start(int32_t max_launches);
+int dsv_timing_stop(float *total_ms, int32_t *launches);
 
 /* Static text for a dsv_status value ("unknown status" otherwise). */
 const char *dsv_status_string(int status);

@@ -1,0 +1,35 @@
+"""MI355X-native verify path of block-diffusion speculative decoding (DScale).
+
+Two operations behind the C ABI of ``libdsv.so`` (declared in
+``include/dsv.h``), with hand-written HIP kernels for gfx950:
+
+* ``verify_attn(q_packed, cu_qlens, kv_pages, page_table, ctx_lens, out)`` --
+  ragged, packed verify attention over a paged bf16 GQA KV cache;
+* ``accept(logits_packed, cu_qlens, draft_tokens, accept_len, next_token)`` --
+  greedy acceptance (per-row vocabulary argmax + longest-prefix compare).
+
+This module only marshals arguments; PyTorch provides device memory and
+streams.  ``Graph`` captures and replays the calls with fixed buffer
+addresses; ``KernelTimer`` times the kernels with HIP events.
+"""
+from ._lib import (  # noqa: F401
+    DSV_BF16,
+    DSV_F32,
+    LIB_PATH,
+    MAX_QLEN,
+    PAGE_SIZE,
+    TIMING_KINDS,
+    AttnDims,
+    DSVError,
+    Graph,
+    KernelTimer,
+    accept,
+    accept_workspace_bytes,
+    alloc_workspace,
+    attn_dims,
+    load,
+    status_string,
+    validate_metadata,
+    verify_attn,
+    verify_attn_workspace_bytes,
+)

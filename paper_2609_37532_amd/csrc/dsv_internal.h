@@ -1,0 +1,77 @@
+// dsv_internal.h -- types and small device helpers shared by the HIP sources
+// of the verify-path library (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dsv.h"
+
+namespace dsv {
+
+// MFMA operand / result vector types (v_mfma_f32_16x16x32_bf16: A and B are
+// 8 bf16 per lane, C/D are 4 fp32 per lane).
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kPage = DSV_PAGE_SIZE;  // tokens per KV page
+constexpr int kMaxQlen = DSV_MAX_QLEN;
+
+// -------------------------------------------------------------------------
+// verify attention
+// -------------------------------------------------------------------------
+struct AttnParams {
+  const uint16_t *q;          // bf16 [cap][Hq][D]
+  const int32_t *cu;          // [B+1]
+  const uint16_t *kv;         // bf16 [P][2][Hkv][16*D]
+  const int32_t *page_table;  // [B][P_max]
+  const int32_t *ctx;         // [B]
+  uint16_t *out;              // bf16 [cap][Hq][D]
+  float *part_o;              // fp32 [S][cap][Hq][D]   (split partials)
+  float2 *part_ml;            // fp32 [S][cap][Hq] x (m, l)
+  int32_t num_reqs, cap, hq, hkv, group, max_pages, num_pages, max_kv_len;
+  int32_t chunk;      // keys per split, multiple of 32
+  int32_t num_splits; // grid extent over splits = ceil(max_kv_len / chunk)
+  float scale_log2;   // softmax scale * log2(e)
+};
+
+// Workspace carve-up shared by the size query and the launcher.
+struct AttnWorkspace {
+  size_t part_o_off, part_ml_off, total;
+};
+
+int32_t attn_split_chunk(const dsv_attn_dims &d);
+AttnWorkspace attn_workspace_layout(const dsv_attn_dims &d);
+hipError_t launch_verify_attn(const AttnParams &p, int head_dim, hipStream_t s);
+
+// -------------------------------------------------------------------------
+// acceptance
+// -------------------------------------------------------------------------
+constexpr int kAcceptChunk = 8192;  // vocabulary elements per argmax workgroup
+
+struct AcceptWorkspace {
+  size_t val_off, idx_off, total;
+  int32_t num_chunks;
+};
+AcceptWorkspace accept_workspace_layout(int32_t cap, int32_t vocab);
+hipError_t launch_accept(const void *logits, int dtype, const int32_t *cu,
+                         const int32_t *draft, int32_t *accept_len,
+                         int32_t *next_token, int32_t num_reqs, int32_t cap,
+                         int32_t vocab, float *best_val, int32_t *best_idx,
+                         int32_t num_chunks, hipStream_t s);
+
+hipError_t launch_validate(const int32_t *cu, const int32_t *ctx,
+                           const int32_t *page_table, const dsv_attn_dims &d,
+                           int32_t *err_word, hipStream_t s);
+
+// Kernel kinds of the timing hook (see dsv_timing_start).
+enum TimingKind { kTimeAttnSplit = 0, kTimeAttnCombine = 1, kTimeArgmax = 2, kTimePrefix = 3 };
+// Records a HIP event before (end = false) or after (end = true) a launch
+// when timing is on and the stream is not being captured.
+void timing_mark(int kind, bool end, hipStream_t s);
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace dsv

@@ -1,0 +1,101 @@
+"""Device-side helpers shared by the GPU tests (marshalling only)."""
+import sys
+
+import numpy as np
+import torch
+
+import paper_2609_37532_amd as dsv
+import workloads as W
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    """Flushed progress line naming the case (survives a dead box)."""
+    print("[gpu-test]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def bf16_dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def i32_dev(a) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(DEV)
+
+
+def bf16_host(t: torch.Tensor) -> np.ndarray:
+    """bf16 device tensor -> float64 numpy (exact)."""
+    bits = t.detach().view(torch.int16).cpu().numpy().view(np.uint16)
+    return W.bf16_to_f32(bits).astype(np.float64)
+
+
+class AttnDev:
+    """An AttnInputs uploaded once; `run()` enqueues verify_attn."""
+
+    def __init__(self, inp: W.AttnInputs, fill_out: float = float("nan")):
+        self.inp = inp
+        self.q = bf16_dev(inp.q)
+        self.cu = i32_dev(inp.cu_qlens)
+        self.kv = bf16_dev(inp.kv_pages)
+        self.pt = i32_dev(inp.page_table)
+        self.ctx = i32_dev(inp.ctx_lens)
+        self.out = torch.full(tuple(inp.q.shape), fill_out, dtype=torch.bfloat16, device=DEV)
+        self.dims = dsv.attn_dims(self.q, self.kv, self.pt, max_kv_len=inp.max_kv_len,
+                                  scale=inp.scale)
+        self.ws = dsv.alloc_workspace(dsv.verify_attn_workspace_bytes(self.dims), DEV)
+
+    def run(self, stream=None):
+        dsv.verify_attn(self.q, self.cu, self.kv, self.pt, self.ctx, self.out,
+                        dims=self.dims, workspace=self.ws, stream=stream)
+
+    def result(self) -> np.ndarray:
+        torch.cuda.synchronize()
+        return bf16_host(self.out)
+
+
+def run_attn(inp: W.AttnInputs) -> np.ndarray:
+    d = AttnDev(inp)
+    d.run()
+    return d.result()
+
+
+def attn_errors(got: np.ndarray, ref: np.ndarray, inp: W.AttnInputs):
+    live = int(inp.cu_qlens[-1])
+    err = np.abs(got[:live] - ref[:live])
+    return float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
+
+
+def assert_attn_close(got, ref, inp, max_abs=1e-2, mean_abs=1e-3):
+    """Tolerance of the verify path: max-abs 1e-2, mean-abs 1e-3 vs fp64;
+    tail rows exactly zero."""
+    live = int(inp.cu_qlens[-1])
+    assert np.isfinite(got).all(), "non-finite output"
+    mx, mn = attn_errors(got, ref, inp)
+    assert mx <= max_abs and mn <= mean_abs, "max %.3g mean %.3g" % (mx, mn)
+    assert not got[live:].any(), "tail rows not zero"
+    return mx, mn
+
+
+class AcceptDev:
+    def __init__(self, acc: W.AcceptInputs):
+        self.acc = acc
+        if acc.dtype == "bf16":
+            self.logits = bf16_dev(acc.logits)
+        else:
+            self.logits = torch.from_numpy(acc.logits).to(DEV)
+        self.cu = i32_dev(acc.cu_qlens)
+        self.draft = i32_dev(acc.draft_tokens)
+        B = acc.num_reqs
+        self.a = torch.full((B,), -7, dtype=torch.int32, device=DEV)
+        self.nxt = torch.full((B,), -7, dtype=torch.int32, device=DEV)
+        self.ws = dsv.alloc_workspace(
+            dsv.accept_workspace_bytes(acc.capacity, B, acc.vocab), DEV)
+
+    def run(self, stream=None):
+        dsv.accept(self.logits, self.cu, self.draft, self.a, self.nxt, workspace=self.ws,
+                   stream=stream)
+
+    def result(self):
+        torch.cuda.synchronize()
+        return self.a.cpu().numpy(), self.nxt.cpu().numpy()

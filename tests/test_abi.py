@@ -1,0 +1,140 @@
+"""The C ABI on the CPU: the library loads, exports every function that
+include/dsv.h declares, and rejects bad host-known arguments with the
+documented status codes before enqueueing anything (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_37532_amd as dsv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dsv.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dsv_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = dsv.load()
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_no_bare_posix_names_exported():
+    # a bare `accept` symbol would interpose accept(2) in the host process
+    out = os.popen("nm -D --defined-only %s" % dsv.LIB_PATH).read()
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    assert "accept" not in exported and "verify_attn" not in exported
+    assert all(n.startswith("dsv_") for n in exported if not n.startswith("_"))
+
+
+def test_status_strings():
+    expect = {0: "ok", -1: "null pointer argument", -2: "dimension out of range",
+              -3: "unsupported configuration",
+              -4: "workspace missing, misaligned or too small", -5: "HIP runtime error",
+              7: "unknown status"}
+    for code, text in expect.items():
+        assert dsv.status_string(code) == text
+
+
+def good_dims(**kw):
+    d = dict(num_reqs=32, capacity=256, num_q_heads=32, num_kv_heads=8, head_dim=128,
+             page_size=16, max_pages_per_req=514, num_pages=10000, max_kv_len=8208,
+             scale=0.08838834764831845)
+    d.update(kw)
+    return dsv.AttnDims(**d)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("num_reqs", 0, -2), ("capacity", 0, -2), ("num_q_heads", 30, -2),
+    ("num_kv_heads", 0, -2), ("max_pages_per_req", 0, -2), ("num_pages", 0, -2),
+    ("max_kv_len", 0, -2), ("max_kv_len", 514 * 16 + 1, -2), ("scale", 0.0, -2),
+    ("scale", float("inf"), -2), ("page_size", 32, -3), ("head_dim", 96, -3),
+    ("num_q_heads", 24, -3),  # G = 3 is not a power of two
+])
+def test_verify_attn_rejects_bad_dims(field, value, status):
+    lib = dsv.load()
+    d = good_dims(**{field: value})
+    assert lib.dsv_verify_attn_workspace_bytes(ctypes.byref(d)) == 0
+    fake = 1 << 20  # never dereferenced: validation fails first
+    rc = lib.dsv_verify_attn(fake, fake, fake, fake, fake, fake, ctypes.byref(d), fake,
+                             1 << 30, None)
+    assert rc == status
+
+
+def test_verify_attn_null_and_workspace_errors():
+    lib = dsv.load()
+    d = good_dims()
+    need = lib.dsv_verify_attn_workspace_bytes(ctypes.byref(d))
+    assert need > 0 and need % 256 == 0
+    fake = 1 << 20
+    assert lib.dsv_verify_attn(None, fake, fake, fake, fake, fake, ctypes.byref(d),
+                               fake, need, None) == -1
+    assert lib.dsv_verify_attn(fake, fake, fake, fake, fake, fake, None, fake, need,
+                               None) == -1
+    # too small, missing, misaligned workspace
+    assert lib.dsv_verify_attn(fake, fake, fake, fake, fake, fake, ctypes.byref(d),
+                               fake, need - 1, None) == -4
+    assert lib.dsv_verify_attn(fake, fake, fake, fake, fake, fake, ctypes.byref(d),
+                               None, need, None) == -4
+    assert lib.dsv_verify_attn(fake, fake, fake, fake, fake, fake, ctypes.byref(d),
+                               fake + 8, need, None) == -4
+
+
+def test_workspace_grows_with_max_kv_len():
+    lib = dsv.load()
+    small = lib.dsv_verify_attn_workspace_bytes(ctypes.byref(good_dims(max_kv_len=1024)))
+    big = lib.dsv_verify_attn_workspace_bytes(ctypes.byref(good_dims(max_kv_len=8208)))
+    assert 0 < small < big
+
+
+def test_accept_rejects_bad_arguments():
+    lib = dsv.load()
+    fake = 1 << 20
+    need = lib.dsv_accept_workspace_bytes(256, 32, 151936)
+    assert need > 0 and need % 256 == 0
+    assert lib.dsv_accept_workspace_bytes(0, 32, 151936) == 0
+    args = [fake, 1, fake, fake, fake, fake, 32, 256, 151936, fake, need, None]
+    bad = list(args); bad[0] = None
+    assert lib.dsv_accept(*bad) == -1
+    bad = list(args); bad[1] = 7
+    assert lib.dsv_accept(*bad) == -3
+    bad = list(args); bad[6] = 0
+    assert lib.dsv_accept(*bad) == -2
+    bad = list(args); bad[8] = 0
+    assert lib.dsv_accept(*bad) == -2
+    bad = list(args); bad[10] = need - 1
+    assert lib.dsv_accept(*bad) == -4
+    bad = list(args); bad[9] = fake + 4
+    assert lib.dsv_accept(*bad) == -4
+
+
+def test_validate_and_graph_and_timing_argument_errors():
+    lib = dsv.load()
+    d = good_dims()
+    fake = 1 << 20
+    assert lib.dsv_validate_metadata(None, fake, fake, ctypes.byref(d), fake, None) == -1
+    bad = good_dims(head_dim=80)
+    assert lib.dsv_validate_metadata(fake, fake, fake, ctypes.byref(bad), fake, None) == -3
+    assert lib.dsv_graph_capture_begin(None) == -1
+    assert lib.dsv_graph_replay(None, None) == -1
+    assert lib.dsv_graph_destroy(None) == -1
+    assert lib.dsv_timing_start(0) == -2
+    assert lib.dsv_timing_stop(None, None) == -1
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    q = torch.zeros(4, 2, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        dsv.verify_attn(q, torch.zeros(2, dtype=torch.int32),
+                        torch.zeros(1, 2, 1, 1024, dtype=torch.bfloat16),
+                        torch.zeros(1, 1, dtype=torch.int32),
+                        torch.zeros(1, dtype=torch.int32), q.clone())

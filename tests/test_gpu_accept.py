@@ -1,0 +1,101 @@
+"""GPU parity of dsv_accept against the oracle: bit-exact accept lengths and
+next tokens (exact argmax with lowest-index ties), through the C ABI."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+try:
+    from gpu_util import AcceptDev, say
+except Exception:  # pragma: no cover
+    pass
+
+
+def check(acc, name):
+    say("accept", name, "B=%d cap=%d V=%d %s" % (acc.num_reqs, acc.capacity, acc.vocab,
+                                                acc.dtype))
+    d = AcceptDev(acc)
+    d.run()
+    a, nxt = d.result()
+    ra, rn = oracle.accept(acc.logits, acc.dtype, acc.cu_qlens, acc.draft_tokens)
+    assert np.array_equal(a, ra), (a, ra)
+    assert np.array_equal(nxt, rn), (nxt, rn)
+    say("accept", name, "ok")
+    return a, nxt
+
+
+def test_tiny_config():
+    attn = W.config_attn_inputs(1)
+    rng = W.config_rng(1)
+    W.config_attn_inputs(1, rng=rng)
+    acc = W.config_accept_inputs(1, attn.cu_qlens, rng)
+    a, nxt = check(acc, "config1")
+    assert np.array_equal(a, acc.planted_accept_len)
+    assert np.array_equal(nxt, acc.planted_next)
+
+
+def test_config4_shape_bf16():
+    attn_rng = W.config_rng(4)
+    attn = W.config_attn_inputs(4, rng=attn_rng)
+    acc = W.config_accept_inputs(4, attn.cu_qlens, attn_rng)
+    a, nxt = check(acc, "config4")
+    assert np.array_equal(a, acc.planted_accept_len)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("vocab", [2, 7, 1000, 1001, 8192, 8193, 20011])
+def test_vocab_sizes_and_alignment(dtype, vocab):
+    # odd vocabularies misalign rows: exercises the scalar head/tail paths
+    rng = np.random.default_rng(vocab)
+    k = np.array([1, 16, 5, 0, 3], np.int32)
+    cu = W.cu_from_lengths(k)
+    acc = W.make_accept_inputs(rng, cu_qlens=cu, capacity=30, vocab=vocab, dtype=dtype,
+                               p_accept=0.4)
+    check(acc, "vocab%d-%s" % (vocab, dtype))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ties_across_chunks_and_lanes(dtype):
+    rng = np.random.default_rng(4)
+    vocab = 3 * 8192 + 100
+    cu = W.cu_from_lengths([4, 4])
+    lg = rng.standard_normal((8, vocab)).astype(np.float32)
+    pairs = [(8191, 8192), (0, vocab - 1), (5, 13), (8192 * 2 + 3, 8192 * 2 + 4),
+             (100, 8192 + 100), (7, 8), (1, 16385), (vocab - 2, vocab - 1)]
+    for r, (p1, p2) in enumerate(pairs):
+        lg[r, p1] = lg[r, p2] = 9.0
+    draft = np.zeros(8, np.int32)
+    logits = W.bf16_bits(lg) if dtype == "bf16" else lg
+    acc = W.AcceptInputs(logits=logits, dtype=dtype, cu_qlens=cu, draft_tokens=draft,
+                         planted_accept_len=np.zeros(2, np.int32),
+                         planted_next=np.zeros(2, np.int32))
+    a, nxt = check(acc, "ties-" + dtype)
+    assert nxt[0] == pairs[0][0] and nxt[1] == pairs[4][0]
+
+
+def test_signed_zero_and_constant_rows():
+    cu = W.cu_from_lengths([3, 2])
+    lg = np.full((5, 300), -1.0, np.float32)
+    lg[0, 40], lg[0, 20] = 0.0, -0.0   # -0 at lower index wins the tie
+    lg[1, :] = 2.5                     # constant row -> index 0
+    lg[2, 299] = 3.0
+    lg[3, 10], lg[3, 9] = -0.0, 0.0
+    draft = np.array([0, 20, 0, 5, 9], np.int32)
+    acc = W.AcceptInputs(logits=lg, dtype="f32", cu_qlens=cu, draft_tokens=draft,
+                         planted_accept_len=np.zeros(2, np.int32),
+                         planted_next=np.zeros(2, np.int32))
+    a, nxt = check(acc, "signed-zero")
+    assert list(a) == [2, 1] and list(nxt) == [299, 0]
+
+
+def test_many_requests_random_drafts():
+    rng = np.random.default_rng(8)
+    k = W.verify_lengths(rng, 64, 512)
+    k[::7] = 0
+    cu = W.cu_from_lengths(k)
+    acc = W.make_accept_inputs(rng, cu_qlens=cu, capacity=int(cu[-1]) + 9, vocab=32000,
+                               dtype="bf16", p_accept=0.2)
+    check(acc, "64-requests")

@@ -1,0 +1,168 @@
+"""GPU parity of dsv_verify_attn against the fp64 oracle (through the C ABI).
+
+Bar: max-abs error <= 1e-2 and mean-abs error <= 1e-3 over live rows, tail
+rows exactly zero, every output finite although every element the kernel
+must not read is NaN (tail q rows, dead slots of last pages, spare pages).
+Invariants that the design makes exact are checked bitwise: packing
+independence, page permutation and run-to-run determinism.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+try:
+    from gpu_util import AttnDev, assert_attn_close, run_attn, say
+except Exception:  # pragma: no cover
+    pass
+
+
+def oracle_out(inp):
+    return oracle.verify_attn(inp.q, inp.cu_qlens, inp.kv_pages, inp.page_table,
+                              inp.ctx_lens, **inp.oracle_kwargs())
+
+
+def case(seed, ctx, qlens, cap=None, hq=32, hkv=8, d=128, **kw):
+    rng = np.random.default_rng(seed)
+    cap = cap if cap is not None else int(sum(qlens)) + 5
+    return W.make_attn_inputs(rng, ctx_lens=ctx, qlens=qlens, capacity=cap,
+                              num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                              spare_pages=3, **kw)
+
+
+def check(inp, name, **tol):
+    say("attn", name, "B=%d k=%s ctx=%s" % (inp.num_reqs, list(inp.qlens)[:8],
+                                           list(inp.ctx_lens)[:8]))
+    got = run_attn(inp)
+    mx, mn = assert_attn_close(got, oracle_out(inp), inp, **tol)
+    say("attn", name, "ok max %.3g mean %.3g" % (mx, mn))
+    return got
+
+
+# ------------------------------------------------------------ the presets
+def test_tiny_config():
+    check(W.config_attn_inputs(1), "config1-tiny")
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_qwen_shaped_configs_all_rows(cfg):
+    check(W.config_attn_inputs(cfg), "config%d" % cfg)
+
+
+def test_config4_all_rows():
+    check(W.config_attn_inputs(4), "config4")
+
+
+# ------------------------------------------------------------ edge cases
+@pytest.mark.parametrize("name,ctx,qlens", [
+    ("decode-k1", [0, 1, 15, 16, 31, 32, 33, 700], [1] * 8),
+    ("full-k16", [0, 5, 16, 17, 100, 511, 512, 513], [16] * 8),
+    ("ragged-mix", [3, 1000, 47, 0, 2048, 9, 130, 600], [5, 1, 16, 2, 7, 13, 3, 9]),
+    ("split-boundaries", [112, 113, 111, 240, 496, 497, 1008, 2032], [16, 15, 1, 16, 16, 15, 16, 16]),
+])
+def test_edge_lengths(name, ctx, qlens):
+    check(case(zlib.crc32(name.encode()) % 1000, ctx, qlens, max_kv_len=4096), name)
+
+
+def test_sentinels_and_tail():
+    inp = case(5, [100, 0, 40, 0, 7], [3, 0, 16, 0, 2], cap=40)
+    check(inp, "sentinels")
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(4, 4, 128), (8, 4, 64), (16, 2, 128), (16, 1, 64),
+                                      (32, 8, 64)])
+def test_head_layouts(hq, hkv, d):
+    check(case(hq * 7 + hkv + d, [300, 17, 64, 1200], [16, 4, 9, 1], hq=hq, hkv=hkv, d=d),
+          "heads-%d-%d-d%d" % (hq, hkv, d))
+
+
+def test_long_context():
+    check(case(77, [16000, 9000, 31], [4, 16, 2], max_kv_len=16384), "long-context")
+
+
+def test_peaked_scores():
+    # Q scaled by 4 makes the softmax peaky; bf16-aware bound.
+    inp = case(91, [800, 50, 2000, 9], [16, 3, 6, 1], q_scale=4.0)
+    say("attn", "peaked")
+    got = run_attn(inp)
+    ref = oracle_out(inp)
+    live = int(inp.cu_qlens[-1])
+    assert np.isfinite(got).all()
+    err = np.abs(got[:live] - ref[:live])
+    assert (err <= 1e-2 + 2.0 ** -8 * np.abs(ref[:live])).all(), float(err.max())
+
+
+def test_closed_form_single_key_is_exact():
+    # ctx = 0, k = 1: one key with weight 1 -> out == V_0 exactly (bf16).
+    inp = case(13, [0, 0, 0], [1, 1, 1])
+    say("attn", "single-key")
+    got = run_attn(inp)
+    ref = oracle_out(inp)
+    live = int(inp.cu_qlens[-1])
+    assert np.array_equal(got[:live], ref[:live])
+
+
+# ------------------------------------------------------------ exact invariants
+def test_packing_independence_bitwise():
+    inp = W.config_attn_inputs(3)
+    say("attn", "packing independence")
+    base = run_attn(inp)
+    B = inp.num_reqs
+    rng = np.random.default_rng(3)
+    for trial in range(2):
+        order = list(rng.permutation(B))
+        gaps = list(rng.integers(0, 2, size=B + 1))
+        alt = W.repack(inp, order, capacity=int(inp.qlens.sum()) + 17, gaps=gaps)
+        got = run_attn(alt)
+        for old_i, new_i, o_old, o_new, k in alt.meta["moves"]:
+            assert np.array_equal(got[o_new:o_new + k], base[o_old:o_old + k]), old_i
+        assert not got[int(alt.cu_qlens[-1]):].any()
+
+
+def test_page_permutation_bitwise():
+    inp = case(29, [900, 41, 3000], [8, 3, 16])
+    say("attn", "page permutation")
+    base = run_attn(inp)
+    perm = np.random.default_rng(5).permutation(inp.num_pages)
+    kv2 = np.empty_like(inp.kv_pages)
+    kv2[perm] = inp.kv_pages
+    pt2 = np.where(inp.page_table >= 0, perm[np.maximum(inp.page_table, 0)], -1)
+    alt = W.AttnInputs(q=inp.q, cu_qlens=inp.cu_qlens, kv_pages=kv2,
+                       page_table=pt2.astype(np.int32), ctx_lens=inp.ctx_lens,
+                       num_q_heads=inp.num_q_heads, num_kv_heads=inp.num_kv_heads,
+                       head_dim=inp.head_dim, page_size=inp.page_size,
+                       max_kv_len=inp.max_kv_len, scale=inp.scale)
+    assert np.array_equal(run_attn(alt), base)
+
+
+def test_determinism_bitwise():
+    inp = W.config_attn_inputs(4)
+    say("attn", "determinism x20")
+    d = AttnDev(inp)
+    d.run()
+    first = d.result()
+    for _ in range(20):
+        d.run()
+    assert np.array_equal(d.result(), first)
+
+
+def test_prefix_stability_within_tolerance():
+    # Row j does not depend on k_i while j < k_i (up to rounding: the work
+    # split changes with the number of live rows).
+    base = case(31, [1500], [16], cap=16)
+    say("attn", "prefix stability")
+    full = run_attn(base)
+    for k in (1, 3, 4, 5, 8, 13):
+        alt = W.AttnInputs(q=base.q, cu_qlens=np.array([0, k], np.int32),
+                           kv_pages=base.kv_pages, page_table=base.page_table,
+                           ctx_lens=base.ctx_lens, num_q_heads=base.num_q_heads,
+                           num_kv_heads=base.num_kv_heads, head_dim=base.head_dim,
+                           page_size=base.page_size, max_kv_len=base.max_kv_len,
+                           scale=base.scale)
+        got = run_attn(alt)
+        assert np.abs(got[:k] - full[:k]).max() <= 2.0 ** -7
