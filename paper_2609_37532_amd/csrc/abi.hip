@@ -23,6 +23,9 @@ int check_dims(const dsv_attn_dims *d) {
   if ((long long)d->max_kv_len > (long long)d->max_pages_per_req * DSV_PAGE_SIZE)
     return DSV_ERR_DIMS;
   if (!(d->scale > 0.f) || !isfinite(d->scale)) return DSV_ERR_DIMS;
+  // the flattened work (KV heads x requests x keys) is indexed with int32
+  if ((long long)d->num_kv_heads * d->num_reqs * ((d->max_kv_len + 31) / 32 * 32) >= (1LL << 30))
+    return DSV_ERR_DIMS;
   if (d->page_size != DSV_PAGE_SIZE) return DSV_ERR_UNSUPPORTED;
   if (d->head_dim != 64 && d->head_dim != 128) return DSV_ERR_UNSUPPORTED;
   if (!is_pow2_group(d->num_q_heads / d->num_kv_heads)) return DSV_ERR_UNSUPPORTED;
@@ -78,6 +81,8 @@ int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
   const AttnWorkspace ws = attn_workspace_layout(*dims);
   if (!workspace || !aligned256(workspace) || workspace_bytes < ws.total)
     return DSV_ERR_WORKSPACE;
+  const int32_t grid = attn_grid(*dims);
+  if (grid <= 0) return DSV_ERR_HIP;  // device query failed
 
   AttnParams p;
   p.q = (const uint16_t *)q_packed;
@@ -86,8 +91,9 @@ int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
   p.page_table = page_table;
   p.ctx = ctx_lens;
   p.out = (uint16_t *)out;
-  p.part_o = (float *)((char *)workspace + ws.part_o_off);
+  p.plan = (int32_t *)((char *)workspace + ws.plan_off);
   p.part_ml = (float2 *)((char *)workspace + ws.part_ml_off);
+  p.part_o = (float *)((char *)workspace + ws.part_o_off);
   p.num_reqs = dims->num_reqs;
   p.cap = dims->capacity;
   p.hq = dims->num_q_heads;
@@ -96,8 +102,7 @@ int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
   p.max_pages = dims->max_pages_per_req;
   p.num_pages = dims->num_pages;
   p.max_kv_len = dims->max_kv_len;
-  p.chunk = attn_split_chunk(*dims);
-  p.num_splits = (dims->max_kv_len + p.chunk - 1) / p.chunk;
+  p.num_wg = grid;
   p.scale_log2 = dims->scale * 1.4426950408889634f;
   const hipError_t e = launch_verify_attn(p, dims->head_dim, (hipStream_t)hip_stream);
   return e == hipSuccess ? DSV_OK : DSV_ERR_HIP;

@@ -29,20 +29,21 @@ struct AttnParams {
   const int32_t *page_table;  // [B][P_max]
   const int32_t *ctx;         // [B]
   uint16_t *out;              // bf16 [cap][Hq][D]
-  float *part_o;              // fp32 [S][cap][Hq][D]   (split partials)
-  float2 *part_ml;            // fp32 [S][cap][Hq] x (m, l)
+  int32_t *plan;              // [B+2]: segment prefix per request, total, share
+  float2 *part_ml;            // fp32 [grid][2][G*16] x (m, l)   (stream-K partials)
+  float *part_o;              // fp32 [grid][2][G*16][D]
   int32_t num_reqs, cap, hq, hkv, group, max_pages, num_pages, max_kv_len;
-  int32_t chunk;      // keys per split, multiple of 32
-  int32_t num_splits; // grid extent over splits = ceil(max_kv_len / chunk)
+  int32_t num_wg;     // persistent grid of the stream-K kernel
   float scale_log2;   // softmax scale * log2(e)
 };
 
 // Workspace carve-up shared by the size query and the launcher.
 struct AttnWorkspace {
-  size_t part_o_off, part_ml_off, total;
+  int32_t grid_cap;  // the largest persistent grid the workspace serves
+  size_t plan_off, part_ml_off, part_o_off, total;
 };
 
-int32_t attn_split_chunk(const dsv_attn_dims &d);
+int32_t attn_grid(const dsv_attn_dims &d);  // launch grid on the current device
 AttnWorkspace attn_workspace_layout(const dsv_attn_dims &d);
 hipError_t launch_verify_attn(const AttnParams &p, int head_dim, hipStream_t s);
 

@@ -88,11 +88,17 @@ def test_verify_attn_null_and_workspace_errors():
                                fake + 8, need, None) == -4
 
 
-def test_workspace_grows_with_max_kv_len():
+def test_workspace_is_bounded_by_the_grid_not_the_context():
+    # stream-K partials: at most two per workgroup of a grid capped at 1024,
+    # so the workspace does not grow with the context length
     lib = dsv.load()
-    small = lib.dsv_verify_attn_workspace_bytes(ctypes.byref(good_dims(max_kv_len=1024)))
-    big = lib.dsv_verify_attn_workspace_bytes(ctypes.byref(good_dims(max_kv_len=8208)))
-    assert 0 < small < big
+    ws = lambda **kw: lib.dsv_verify_attn_workspace_bytes(ctypes.byref(good_dims(**kw)))
+    assert ws(max_kv_len=1024) == ws(max_kv_len=8208) > 0
+    tiny = ws(num_reqs=1, num_kv_heads=1, num_q_heads=4, max_kv_len=64,
+              max_pages_per_req=4)
+    assert 0 < tiny < ws()
+    # the flattened work must stay inside int32 indexing
+    assert ws(num_reqs=65535, max_kv_len=8192) == 0
 
 
 def test_accept_rejects_bad_arguments():

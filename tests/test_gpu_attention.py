@@ -3,8 +3,8 @@
 Bar: max-abs error <= 1e-2 and mean-abs error <= 1e-3 over live rows, tail
 rows exactly zero, every output finite although every element the kernel
 must not read is NaN (tail q rows, dead slots of last pages, spare pages).
-Invariants that the design makes exact are checked bitwise: packing
-independence, page permutation and run-to-run determinism.
+Invariants that the design makes exact are checked bitwise (page
+permutation, run-to-run determinism); packing independence within tolerance.
 """
 import zlib
 
@@ -108,7 +108,11 @@ def test_closed_form_single_key_is_exact():
 
 
 # ------------------------------------------------------------ exact invariants
-def test_packing_independence_bitwise():
+def test_packing_independence():
+    # The same requests packed in another order, with sentinels and another
+    # capacity, give the same rows (within the tolerance: the stream-K share
+    # boundaries depend on the batch's total work, so the fp32 merge order of
+    # a request can change with the packing).
     inp = W.config_attn_inputs(3)
     say("attn", "packing independence")
     base = run_attn(inp)
@@ -120,7 +124,8 @@ def test_packing_independence_bitwise():
         alt = W.repack(inp, order, capacity=int(inp.qlens.sum()) + 17, gaps=gaps)
         got = run_attn(alt)
         for old_i, new_i, o_old, o_new, k in alt.meta["moves"]:
-            assert np.array_equal(got[o_new:o_new + k], base[o_old:o_old + k]), old_i
+            d = np.abs(got[o_new:o_new + k] - base[o_old:o_old + k])
+            assert d.max() <= 2.0 ** -7, (old_i, d.max())
         assert not got[int(alt.cu_qlens[-1]):].any()
 
 
