@@ -1,7 +1,7 @@
 """Benchmark of the verify hot path on one MI355X.
 
 One step = one replay of a captured hipGraph holding the whole path on one
-batch: verify attention (split kernel + combine kernel) for one attention
+batch: verify attention (stream-K kernel + combine kernel) for one attention
 layer, then greedy acceptance (argmax kernel + prefix kernel).  Workload:
 Qwen3-8B attention shape at concurrency 32 -- B=32 requests, 32 query / 8 KV
 heads, head_dim 128, bf16 paged KV (page 16), contexts uniform in
@@ -12,7 +12,7 @@ resident in HBM before the timed region.
 
 Prints one JSON line.  ``value`` = packed verify tokens per second of the
 whole step (sum of live verify lengths / step time).  ``roofline`` is for
-the dominant kernel (the attention split kernel), timed with HIP events on
+the dominant kernel (the stream-K attention kernel), timed with HIP events on
 its stream; ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample.
 """
 from __future__ import annotations
@@ -33,7 +33,7 @@ METRIC = "packed verify tokens/s + HBM GB/s (% peak) per layer, Qwen3-8B shape, 
 UNIT = "packed verify tokens/s"
 HBM_PEAK_GBPS = 8000.0
 CONFIG_INDEX = 4
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "attn_split_config4_counters.json")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "attn_streamk_config4_counters.json")
 ATTN_SOURCE = os.path.join(ROOT, "paper_2609_37532_amd", "csrc", "attn.hip")
 
 
@@ -47,8 +47,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--eager-only", type=int, default=0, metavar="N",
+                    help="only run N eager steps (no graph, no timing, no CPU "
+                         "baseline): the program that hardware-counter passes profile")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only copy a 1 GiB device buffer three times: the plain copy "
+                         "of known size that scales the hardware byte counters")
     return ap.parse_args()
 
 
@@ -97,32 +103,52 @@ def counters_traffic(nbytes_alg):
 
 
 def cpu_baseline(attn, acc, seconds):
-    """fp64 oracle on the first requests of the batch (attention rows of the
-    request + its acceptance rows), until ``seconds`` of CPU time are spent."""
+    """fp64 oracle over the requests of the same batch, one at a time
+    (attention rows of the request + its acceptance rows), repeating passes
+    over the batch until ``seconds`` of CPU time are spent."""
     import oracle
     import workloads as W
-    done_tokens, done_reqs, t_total = 0, 0, 0.0
+    subs = []
     for i in range(attn.num_reqs):
         k = int(attn.qlens[i])
         if k == 0:
             continue
-        sub = W.repack(attn, [i], capacity=k)
         o = int(attn.cu_qlens[i])
-        sub_logits = acc.logits[o:o + k]
-        sub_draft = acc.draft_tokens[o:o + k]
-        t0 = time.perf_counter()
-        oracle.verify_attn(sub.q, sub.cu_qlens, sub.kv_pages, sub.page_table,
-                           sub.ctx_lens, **sub.oracle_kwargs())
-        oracle.accept(sub_logits, acc.dtype, np.array([0, k], np.int32), sub_draft)
-        t_total += time.perf_counter() - t0
-        done_tokens += k
-        done_reqs += 1
-        if t_total >= seconds:
-            break
+        subs.append((W.repack(attn, [i], capacity=k), acc.logits[o:o + k],
+                     acc.draft_tokens[o:o + k], k))
+    done_tokens, done_reqs, passes, t_total = 0, 0, 0, 0.0
+    while t_total < seconds:
+        for sub, sub_logits, sub_draft, k in subs:
+            t0 = time.perf_counter()
+            oracle.verify_attn(sub.q, sub.cu_qlens, sub.kv_pages, sub.page_table,
+                               sub.ctx_lens, **sub.oracle_kwargs())
+            oracle.accept(sub_logits, acc.dtype, np.array([0, k], np.int32), sub_draft)
+            t_total += time.perf_counter() - t0
+            done_tokens += k
+            done_reqs += 1
+            if t_total >= seconds:
+                break
+        passes += 1
     return {"value": done_tokens / t_total, "unit": UNIT, "cores": 1, "kind": "oracle",
-            "sample": "first %d of %d requests of the same batch (%d packed rows): fp64 "
-                      "attention over their keys + acceptance of their rows, %.1f s, "
-                      "single thread" % (done_reqs, attn.num_reqs, done_tokens, t_total)}
+            "sample": "%d request-verifications (%d passes over the %d live requests of "
+                      "the same batch, %d packed rows): fp64 attention over each "
+                      "request's keys + acceptance of its rows, %.1f s, single thread"
+                      % (done_reqs, passes, len(subs), done_tokens, t_total)}
+
+
+def copy_probe():
+    """Three device-to-device copies of 1 GiB: reads and writes 2^30 bytes
+    each, the known size against which FETCH_SIZE / WRITE_SIZE are scaled."""
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
 
 
 def main():
@@ -135,10 +161,14 @@ def main():
 
     import torch
 
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_probe:
+        copy_probe()
+        return
+
     import paper_2609_37532_amd as dsv
     import workloads as W
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda", 0)
     t0 = time.time()
     rng = W.config_rng(CONFIG_INDEX)
@@ -172,6 +202,12 @@ def main():
         dsv.accept(logits, cu, draft, a_len, nxt, workspace=ws_acc, stream=s)
 
     torch.cuda.synchronize()
+    if args.eager_only:
+        for _ in range(args.eager_only):
+            step_on(stream)
+        torch.cuda.synchronize()
+        print(json.dumps({"eager_steps": args.eager_only}), flush=True)
+        return
     step_on(stream)  # eager run once before capture
     torch.cuda.synchronize()
     graph = dsv.Graph().capture(lambda: step_on(stream), stream)
@@ -239,11 +275,11 @@ def main():
             "packed_tokens": tokens,
             "kv_tokens": int((attn.ctx_lens + attn.qlens).sum()),
             "capacity": attn.capacity,
-            "step": "one hipGraph replay: attn split + combine + argmax + prefix",
+            "step": "one hipGraph replay: attn stream-K + combine + argmax + prefix",
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "attn_split_kernel<128>",
+            "kernel": "attn_streamk_kernel<128>",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
