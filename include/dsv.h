@@ -26,10 +26,11 @@
  *    returned.  The library never aborts the process.
  *  - Device-resident metadata (cu_qlens, ctx_lens, page_table, draft_tokens)
  *    cannot be validated on the host without a synchronisation.  The kernels
- *    re-check it cheaply: a request whose metadata breaks a precondition
- *    below is skipped (its outputs are left untouched), a page id outside
- *    [0, num_pages) is never dereferenced, and no access leaves the buffers
- *    described here.  dsv_validate_metadata reports such violations.
+ *    re-check it cheaply: a request whose offsets or lengths break a
+ *    precondition below is skipped (its outputs are left untouched); a page
+ *    id outside [0, num_pages) is never dereferenced (page 0 is read in its
+ *    place, so that request's output is unspecified); no access leaves the
+ *    buffers described here.  dsv_validate_metadata reports such violations.
  *  - Notation: B = num_reqs, G = num_q_heads / num_kv_heads (GQA group),
  *    D = head_dim, k_i = cu_qlens[i+1] - cu_qlens[i] = verify length of
  *    request i (1 anchor + k_i - 1 drafted candidates; 0 for a sentinel
@@ -76,8 +77,7 @@ typedef enum { DSV_F32 = 0, DSV_BF16 = 1 } dsv_dtype;
  *  max_pages_per_req P_max >= 1, the row stride of page_table.
  *  num_pages         pages in kv_pages; page ids must lie in [0, num_pages).
  *  max_kv_len        an upper bound on ctx_lens[i] + k_i over every call that
- *                    uses the same workspace (it sizes the split partials),
- *                    1 <= max_kv_len <= P_max * 16.
+ *                    uses the same dims, 1 <= max_kv_len <= P_max * 16.
  *  scale             softmax scale applied to q.k (normally 1/sqrt(D)).
  */
 typedef struct {
@@ -95,9 +95,12 @@ typedef struct {
 
 /*
  * Workspace bytes dsv_verify_attn needs for `dims` (0 if dims are invalid).
- * The workspace holds the fp32 split-KV partials; it needs no initialisation
- * and its contents after a call are unspecified.  Its address may stay fixed
- * across steps (Eq. (13)), so a captured graph can be replayed.
+ * The workspace holds the work plan and the fp32 partial results (O, m, l) of
+ * the (request, KV head) segments that the persistent grid splits between
+ * workgroups: at most two per workgroup of a grid of at most 1024, so its
+ * size does not grow with max_kv_len.  It needs no initialisation and its
+ * contents after a call are unspecified.  Its address may stay fixed across
+ * steps (Eq. (13)), so a captured graph can be replayed.
  */
 size_t dsv_verify_attn_workspace_bytes(const dsv_attn_dims *dims);
 
@@ -139,9 +142,11 @@ size_t dsv_verify_attn_workspace_bytes(const dsv_attn_dims *dims);
  * Precision: q.k products, the softmax and all accumulation are fp32; the
  * softmax weights enter the weighted sum of V rounded to bf16 (and the same
  * rounded weights form the normaliser); `out` is rounded once to bf16
- * (round-to-nearest-even).  The result for a request is deterministic and
- * does not depend on how the other requests are packed or on which physical
- * pages hold its keys.
+ * (round-to-nearest-even).  Results are bitwise deterministic for given
+ * inputs and do not depend on which physical pages hold the keys.  How the
+ * other requests are packed changes a request's result only through the
+ * summation order (the work split follows the batch's total work), i.e.
+ * within rounding.
  */
 int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
                     const void *kv_pages, const int32_t *page_table,

@@ -23,20 +23,21 @@
 //    per workgroup.  Results depend only on the request's own data and the
 //    batch's total work (the share size), and merge in a fixed order, so
 //    they are deterministic.
+//  * K/V stream through an LDS ring of four 32-key blocks filled by
+//    LDS-direct loads three blocks ahead; each wave loads one 4 KiB tile
+//    per block (one page's K or V) as four contiguous 1 KiB loads from a
+//    scalar page address, so the loop spends almost no vector or scalar
+//    instructions on addressing.  Page ids are staged in LDS per piece.
 //  * Transposed scores: S^T = K Q^T and O^T = V^T P^T with
 //    v_mfma_f32_16x16x32_bf16.  The score tile comes out with one query row
 //    per lane column, which is exactly the B-operand layout the PV product
-//    needs, so P never crosses lanes; the row max needs two xor shuffles.
-//  * Every MFMA operand is one direct global load per lane: the K tile is
-//    stored in 8-wide d chunks (a wave reads 1 KiB contiguous per load) and
-//    the V tile d-major (each lane reads the 4 consecutive keys it
-//    multiplies).  One operand buffer per wave, reused in place: the next
-//    32-key block's K is loaded as soon as the score MFMAs have consumed the
-//    current K, its V as soon as the PV MFMAs have consumed the current V.
-//    Page ids are fetched 64 at a time into a lane-indexed register and read
-//    with v_readlane, so no page-table load sits in front of a K/V load.
-//  * Waves of a workgroup split the keys when a request has few row tiles and
-//    merge through LDS; with three or more row tiles each wave owns tiles.
+//    needs, so P never crosses lanes; the row max needs two row-swap
+//    permutes, and the row sum is one more MFMA against a tile of ones.
+//  * Lazy rescaling: the running maximum only moves (and the accumulators
+//    are only rescaled) when a block's maximum exceeds it by more than a
+//    factor 2^8, which keeps the weights below 2^8.
+//  * Waves of a workgroup split the dims when a request has one or two row
+//    tiles; with three or more row tiles each wave owns tiles.
 #include "dsv_internal.h"
 
 #include <math.h>
@@ -52,20 +53,11 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
-__device__ __forceinline__ float shfl_xor_f(float x, int m) {
-  return __shfl_xor(x, m, kWave);
-}
-
 // Two bf16 -> one uint32 (low half first), round to nearest even.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   __bf16 a = (__bf16)lo, b = (__bf16)hi;
   return (uint32_t)__builtin_bit_cast(uint16_t, a) |
          ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
-}
-
-__device__ __forceinline__ float bf16_round(float x) {
-  __bf16 a = (__bf16)x;
-  return (float)a;
 }
 
 __device__ __forceinline__ int round_up_block(int x) {
@@ -106,20 +98,24 @@ __device__ __forceinline__ ReqMeta load_req(const AttnParams &p, int i) {
 }
 
 // ------------------------------------------------------------------ LDS ring
-// One 32-key block in LDS holds the MFMA operand tiles of K (two 16-key
-// score halves x D/32 chunks of 32 dims) and of V (D/16 blocks of 16 dims),
-// 1 KiB each and stored in lane order: lane l's 16 bytes sit at l*16, so a
-// wave reads an operand with one conflict-free ds_read_b128 and a ring load
-// (global_load_lds_dwordx4, written by each lane at its own slot) fills one.
+// One 32-key block (two pages) in LDS: the K tiles of both pages, then their
+// V tiles, each tile as D/32 chunks of 1 KiB.  A wave fills one tile per
+// block with D/32 LDS-direct loads (global_load_lds_dwordx4): page
+// wave & 1, K for waves 0-1 and V for waves 2-3.  Each load reads one
+// contiguous KiB of the tile; lane l writes the 16 bytes at offset 16*l of
+// the chunk and fetches a swizzled 16-byte unit of it (each aligned group of
+// four lanes still fetches one aligned 64-byte piece), chosen so that the
+// MFMA operand reads are free of LDS bank conflicts for any grouping of 8,
+// 16 or 32 lanes per LDS cycle (k_unit / v_unit below).
 template <int D>
-struct RingShape {
-  static constexpr int kKOps = 2 * (D / 32);
-  static constexpr int kVOps = D / 16;
-  static constexpr int kOps = kKOps + kVOps;          // 16 at D = 128
-  static constexpr int kOpsPerWave = kOps / kWaves;   // ring loads per wave per block
+struct Ring {
+  static constexpr int kChunks = D / 32;               // 1 KiB chunks per tile
+  static constexpr int kKRegion = 2 * kChunks * 1024;  // K tiles of both pages
+  static constexpr int kStage = 2 * kKRegion;          // 16 KiB at D = 128
+  static constexpr int kKOps = 2 * kChunks;            // K operand tiles per block
 };
 constexpr int kStages = 4;      // blocks resident in the ring (3 in flight)
-constexpr int kSubPages = 128;  // page ids staged in LDS at a time (2048 keys)
+constexpr int kSubPages = 512;  // page ids staged in LDS at a time (8192 keys)
 
 // s_waitcnt immediate (gfx9 encoding): wait until at most `vm` vector-memory
 // and `lgkm` LDS/scalar operations of this wave are outstanding.
@@ -132,136 +128,129 @@ constexpr int waitcnt_imm(int vm, int lgkm) {
 // what must be complete first.
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// Ring operand reads.  One inline-asm block issues the ds_read_b128 of all
-// K (or all V) operand tiles of a stage and waits for them, so its outputs
-// exist only once the data is in registers.  Asm, because the compiler cannot
-// tell ring stages apart and would otherwise wait for every ring load in
-// flight before each read; the stage read here is complete by construction
-// (explicit wait + barrier at the top of the step).  `base` is the LDS
-// address of this lane's slot in the stage (stage + lane * 16).
+// The wave's LDS-direct loads of one block: the D/32 chunks of one tile at
+// `src` (uniform) into LDS at byte address `dst` (uniform).  The immediate
+// offset applies to both the global and the LDS address.  In asm so that
+// the compiler, which cannot tell ring stages apart, does not make its own
+// LDS reads wait for every ring load in flight; the explicit waits in
+// ring_step order them instead.
 template <int D>
-struct RingRead;
+__device__ __forceinline__ void ring_dma(uint32_t dst, uint32_t voff, const void *src);
 
 template <>
-struct RingRead<128> {
-  static __device__ __forceinline__ void k(uint32_t base, uint4 (&o)[8]) {
-    asm volatile(
-        "ds_read_b128 %0, %8\n\tds_read_b128 %1, %8 offset:1024\n\t"
-        "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
-        "ds_read_b128 %4, %8 offset:4096\n\tds_read_b128 %5, %8 offset:5120\n\t"
-        "ds_read_b128 %6, %8 offset:6144\n\tds_read_b128 %7, %8 offset:7168\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]),
-          "=&v"(o[6]), "=&v"(o[7])
-        : "v"(base)
-        : "memory");
-  }
-};
+__device__ __forceinline__ void ring_dma<128>(uint32_t dst, uint32_t voff, const void *src) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "global_load_lds_dwordx4 %1, %2 offset:0\n\t"
+      "global_load_lds_dwordx4 %1, %2 offset:1024\n\t"
+      "global_load_lds_dwordx4 %1, %2 offset:2048\n\t"
+      "global_load_lds_dwordx4 %1, %2 offset:3072" ::"s"(dst),
+      "v"(voff), "s"(src)
+      : "memory", "m0");
+}
 
 template <>
-struct RingRead<64> {
-  static __device__ __forceinline__ void k(uint32_t base, uint4 (&o)[4]) {
-    asm volatile(
-        "ds_read_b128 %0, %4\n\tds_read_b128 %1, %4 offset:1024\n\t"
-        "ds_read_b128 %2, %4 offset:2048\n\tds_read_b128 %3, %4 offset:3072\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3])
-        : "v"(base)
-        : "memory");
-  }
-};
-
-// The first `n` (1, 2, 4 or 8) V operand tiles starting at LDS address
-// `base`, read and waited for in one asm block.
-template <int N>
-__device__ __forceinline__ void ring_read_v(uint32_t base, uint4 (&o)[8]) {
-  if constexpr (N == 1) {
-    asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-                 : "=&v"(o[0]) : "v"(base) : "memory");
-  } else if constexpr (N == 2) {
-    asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %2 offset:1024\n\t"
-                 "s_waitcnt lgkmcnt(0)"
-                 : "=&v"(o[0]), "=&v"(o[1]) : "v"(base) : "memory");
-  } else if constexpr (N == 4) {
-    asm volatile("ds_read_b128 %0, %4\n\tds_read_b128 %1, %4 offset:1024\n\t"
-                 "ds_read_b128 %2, %4 offset:2048\n\tds_read_b128 %3, %4 offset:3072\n\t"
-                 "s_waitcnt lgkmcnt(0)"
-                 : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]) : "v"(base) : "memory");
-  } else {
-    asm volatile(
-        "ds_read_b128 %0, %8\n\tds_read_b128 %1, %8 offset:1024\n\t"
-        "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
-        "ds_read_b128 %4, %8 offset:4096\n\tds_read_b128 %5, %8 offset:5120\n\t"
-        "ds_read_b128 %6, %8 offset:6144\n\tds_read_b128 %7, %8 offset:7168\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]),
-          "=&v"(o[6]), "=&v"(o[7])
-        : "v"(base)
-        : "memory");
-  }
+__device__ __forceinline__ void ring_dma<64>(uint32_t dst, uint32_t voff, const void *src) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "global_load_lds_dwordx4 %1, %2 offset:0\n\t"
+      "global_load_lds_dwordx4 %1, %2 offset:1024" ::"s"(dst),
+      "v"(voff), "s"(src)
+      : "memory", "m0");
 }
 
 // Key order inside a block.  Row m of score half hh holds key
 // 8*(m/4) + 4*hh + m%4, so after S^T = K Q^T the lane with k-group kq holds
 // keys 8*kq + [0..7] of its query row: exactly the order the PV product
 // contracts over, and V's operand for that lane is 8 consecutive keys of one
-// dim, one 16-byte read of the d-major V tile.
+// dim, one 16-byte unit of the d-major V tile.
 __device__ __forceinline__ int score_key(int hh, int m) { return 8 * (m >> 2) + 4 * hh + (m & 3); }
 
-// Issues this wave's share of the ring loads of one block (pages pid0,
-// pid1) into `stage`.  An invalid page id reads the start of the pool
-// instead (a valid address); the compute step masks those keys.
-template <int D>
-__device__ __forceinline__ void ring_load(const AttnParams &p, int g, int pid0, int pid1,
-                                          uint4 (*stage)[kWave], int wave, int lane) {
-  using R = RingShape<D>;
-  const int m = lane & 15, kgrp = lane >> 4;
-  const bool ok0 = (unsigned)pid0 < (unsigned)p.num_pages;
-  const bool ok1 = (unsigned)pid1 < (unsigned)p.num_pages;
-  const size_t tile = (size_t)kPage * D;
-  const uint16_t *k0 = p.kv + (ok0 ? ((size_t)pid0 * 2 * p.hkv + g) * tile : 0);
-  const uint16_t *k1 = p.kv + (ok1 ? ((size_t)pid1 * 2 * p.hkv + g) * tile : 0);
-  const uint16_t *v0 = k0 + (ok0 ? (size_t)p.hkv * tile : 0);
-  const uint16_t *v1 = k1 + (ok1 ? (size_t)p.hkv * tile : 0);
-#pragma unroll
-  for (int u = 0; u < R::kOpsPerWave; ++u) {
-    const int op = wave * R::kOpsPerWave + u;
-    const uint16_t *src;
-    if (op < R::kKOps) {
-      const int hh = op / (D / 32), c = op % (D / 32);
-      const int key = score_key(hh, m);
-      src = (key < 16 ? k0 : k1) + ((4 * c + kgrp) * 16 + (key & 15)) * 8;
-    } else {
-      const int e = op - R::kKOps;
-      src = (kgrp >= 2 ? v1 : v0) + (16 * e + m) * 16 + 8 * (kgrp & 1);
-    }
-    __builtin_amdgcn_global_load_lds(src, &stage[op][0], 16, 0, 0);
-  }
+// Swizzles.  K chunk of page p: global unit u (d-chunk u/16, slot u%16)
+// sits at LDS unit k_unit(u, p) (an involution).  V chunk: global unit
+// u = 2*dim + half sits at LDS unit v_unit(u); v_unit_inv is its inverse.
+__device__ __forceinline__ int k_unit(int u, int p) { return u ^ (4 * (p ^ ((u >> 3) & 1))); }
+__device__ __forceinline__ int v_sel(int k) { return ((k >> 1) ^ (k >> 2)) & 1; }
+__device__ __forceinline__ int v_unit(int u) {
+  const int k = u >> 2, j = (u >> 1) & 1, b = u & 1;
+  return 4 * k + 2 * (b ^ v_sel(k)) + j;
+}
+__device__ __forceinline__ int v_unit_inv(int l) {
+  const int k = l >> 2, j = l & 1, b = ((l >> 1) & 1) ^ v_sel(k);
+  return 4 * k + 2 * j + b;
 }
 
-// Online-softmax state of one lane: one query row (lane & 15) and, for each
-// of the wave's d blocks u (dims 16*(e_lo+u) + 4*(lane>>4) + [0..3]), the 4
-// accumulated outputs.
+// Per-lane LDS byte offsets (within a stage) of the MFMA operands.
+struct RingLane {
+  uint32_t k0, k1;  // K operand, score half 0 / 1, chunk 0 (chunk c at +1024c)
+  uint32_t v;       // V operand of d block 0 (d block e at +512e)
+};
+
+template <int D>
+__device__ __forceinline__ RingLane ring_lane(int lane) {
+  using R = Ring<D>;
+  const int kgrp = lane >> 4, m = lane & 15;
+  RingLane r;
+  {
+    const int key0 = score_key(0, m), key1 = score_key(1, m);
+    const int p0 = key0 >> 4, p1 = key1 >> 4;
+    r.k0 = (uint32_t)(p0 * R::kChunks * 1024 + 16 * k_unit(kgrp * 16 + (key0 & 15), p0));
+    r.k1 = (uint32_t)(p1 * R::kChunks * 1024 + 16 * k_unit(kgrp * 16 + (key1 & 15), p1));
+  }
+  {
+    // dim m of d block 0, keys 8*(kgrp&1) .. +7 of page kgrp>>1
+    const int pv = kgrp >> 1;
+    r.v = (uint32_t)(R::kKRegion + pv * R::kChunks * 1024 + 16 * v_unit(2 * m + (kgrp & 1)));
+  }
+  return r;
+}
+
+// Maximum / sum over the four lanes that hold one query row (lanes n, n+16,
+// n+32, n+48), with the gfx950 row-swap permutes.
+__device__ __forceinline__ float row_max4(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+// The running maximum is only raised when a block's maximum exceeds it by
+// more than this (base-2 units): weights then stay below 2^8, and the
+// accumulators are rescaled only on such a jump instead of every block.
+constexpr float kRescaleSlack = 8.f;
+
+// Online-softmax state of one lane: one query row (lane & 15); `lacc` holds
+// the row sum of the weights (every element, from an MFMA against ones);
+// for each of the wave's d blocks u (dims 16*(e_lo+u) + 4*(lane>>4) +
+// [0..3]), the 4 accumulated outputs.
 template <int D>
 struct RowState {
-  float m, l;
+  float m;
+  f32x4 lacc;
   f32x4 o[D / 16];
 };
 
-// One 32-key block from the ring: scores for the wave's row tile, online
-// softmax, and the PV product for the wave's `ne` d blocks starting at e_lo.
-// `full` (uniform) says every key of the block is visible to every live row
-// and both pages are valid, so no masking is needed.
+// One 32-key block from ring stage byte offset `so`: scores for the wave's
+// row tile, online softmax, and the PV product for the wave's NE d blocks
+// starting at e_lo (`vb` already points at e_lo).  `full` (uniform) says every
+// key of the block is visible to every live row, so no masking is needed.
 template <int D, int NE>
-__device__ __forceinline__ void ring_compute(const uint4 (*stage)[kWave], int lane, int t0,
-                                             int key_end, int row_limit, bool full, bool ok0,
-                                             bool ok1, const bf16x8 (&qv)[D / 32], int e_lo,
-                                             float scale_log2, RowState<D> &st) {
-  using R = RingShape<D>;
+__device__ __forceinline__ void ring_compute(const char *ring, uint32_t so, const RingLane &rl,
+                                             uint32_t vb, int lane, int t0, int key_end,
+                                             int row_limit, bool full,
+                                             const bf16x8 (&qv)[D / 32], float scale_log2,
+                                             RowState<D> &st) {
+  using R = Ring<D>;
   const int kq = lane >> 4;
-  const uint32_t base = (uint32_t)(uintptr_t)&stage[0][lane];  // LDS offset: low half
   uint4 kop[R::kKOps];
-  RingRead<D>::k(base, kop);
+#pragma unroll
+  for (int c = 0; c < R::kChunks; ++c) {
+    kop[c] = *reinterpret_cast<const uint4 *>(ring + so + rl.k0 + 1024 * c);
+    kop[R::kChunks + c] = *reinterpret_cast<const uint4 *>(ring + so + rl.k1 + 1024 * c);
+  }
+  uint4 vop[NE];
+#pragma unroll
+  for (int u = 0; u < NE; ++u) vop[u] = *reinterpret_cast<const uint4 *>(ring + so + vb + 512 * u);
   f32x4 s[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -271,55 +260,53 @@ __device__ __forceinline__ void ring_compute(const uint4 (*stage)[kWave], int la
       s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kop[h * (D / 32) + c]), qv[c],
                                                      s[h], 0, 0, 0);
   }
-  // element (h, q) of this lane is key t0 + 8kq + 4h + q, in page kq / 2
-  const bool page_ok = kq >= 2 ? ok1 : ok0;
+  // element (h, q) of this lane is key t0 + 8kq + 4h + q; raw scores (the
+  // scale is positive and applied inside the exponent)
   float sc[2][4];
   if (full) {
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) sc[h][q] = s[h][q] * scale_log2;
+      for (int q = 0; q < 4; ++q) sc[h][q] = s[h][q];
   } else {
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int t = t0 + 8 * kq + 4 * h + q;
-        const bool vis = t <= row_limit && t < key_end && page_ok;
-        sc[h][q] = vis ? s[h][q] * scale_log2 : -INFINITY;
+        const bool vis = t <= row_limit && t < key_end;
+        sc[h][q] = vis ? s[h][q] : -INFINITY;
       }
   }
   float bmax = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
                      fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
-  bmax = fmaxf(bmax, shfl_xor_f(bmax, 16));
-  bmax = fmaxf(bmax, shfl_xor_f(bmax, 32));
-  const float m_new = fmaxf(st.m, bmax);
-  const float m_use = m_new == -INFINITY ? 0.f : m_new;
-  const float alpha = __builtin_amdgcn_exp2f(st.m - m_use);
-  // P in bf16 (the PV operand); the row sum uses the same rounded weights so
-  // the normalisation matches what multiplies V.
+  bmax = row_max4(bmax) * scale_log2;
+  if (__builtin_amdgcn_ballot_w64(bmax > st.m + kRescaleSlack) != 0) {
+    const float m_new = fmaxf(st.m, bmax);
+    // 0 on a row's first visible block, 1 for a row that still sees nothing
+    const float alpha = __builtin_amdgcn_exp2f(st.m - (m_new == -INFINITY ? 0.f : m_new));
+    st.lacc *= alpha;
+#pragma unroll
+    for (int u = 0; u < NE; ++u) st.o[u] *= alpha;
+    st.m = m_new;
+  }
+  const float neg_m = st.m == -INFINITY ? 0.f : -st.m;
+  // P in bf16 (the PV operand); the row sum uses the same rounded weights
   uint32_t pk[4];
-  float psum = 0.f;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const float p0 = bf16_round(__builtin_amdgcn_exp2f(sc[h][0] - m_use));
-    const float p1 = bf16_round(__builtin_amdgcn_exp2f(sc[h][1] - m_use));
-    const float p2 = bf16_round(__builtin_amdgcn_exp2f(sc[h][2] - m_use));
-    const float p3 = bf16_round(__builtin_amdgcn_exp2f(sc[h][3] - m_use));
-    psum += (p0 + p1) + (p2 + p3);
+    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][0], scale_log2, neg_m));
+    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][1], scale_log2, neg_m));
+    const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][2], scale_log2, neg_m));
+    const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][3], scale_log2, neg_m));
     pk[2 * h] = pack_bf16x2(p0, p1);
     pk[2 * h + 1] = pack_bf16x2(p2, p3);
   }
-  st.l = st.l * alpha + psum;
-  st.m = m_new;
   const bf16x8 pb = as_bf16x8(make_uint4(pk[0], pk[1], pk[2], pk[3]));
-  // O^T += V^T P^T over this wave's d blocks.  V element q of this lane is
-  // key t0 + 8kq + q.  Keys at or past key_end, and keys of an invalid page,
+  // V element q of this lane is key t0 + 8kq + q.  Keys at or past key_end
   // may hold anything (even NaN): zero their V so that 0 * V stays 0.
-  uint4 vop[8];
-  ring_read_v<NE>(base + (R::kKOps + e_lo) * 1024, vop);
   if (!full) {
-    const int tb = page_ok ? t0 + 8 * kq : key_end;
+    const int tb = t0 + 8 * kq;
     uint32_t vmask[4];
 #pragma unroll
     for (int w = 0; w < 4; ++w)
@@ -333,11 +320,11 @@ __device__ __forceinline__ void ring_compute(const uint4 (*stage)[kWave], int la
       vop[u].w &= vmask[3];
     }
   }
+  const uint4 ones = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
+  st.lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ones), pb, st.lacc, 0, 0, 0);
 #pragma unroll
-  for (int u = 0; u < NE; ++u) {
-    st.o[u] *= alpha;
+  for (int u = 0; u < NE; ++u)
     st.o[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vop[u]), pb, st.o[u], 0, 0, 0);
-  }
 }
 
 // Writes a finished row tile for the wave's `ne` d blocks from e_lo: bf16
@@ -348,7 +335,7 @@ __device__ __forceinline__ void ring_compute(const uint4 (*stage)[kWave], int la
 template <int D>
 __device__ __forceinline__ void write_tile(const AttnParams &p, int g, bool complete, int slot,
                                            const ReqMeta &rq, int rt, int e_lo, int ne,
-                                           int lane, const RowState<D> &st) {
+                                           int lane, float l, const RowState<D> &st) {
   const int kq = lane >> 4, n = lane & 15;
   const int rr = rt * 16 + n;
   if (rr >= p.group * rq.k) return;
@@ -356,7 +343,7 @@ __device__ __forceinline__ void write_tile(const AttnParams &p, int g, bool comp
   const int j = rr >> lg, hh = rr & (p.group - 1);
   if (complete) {
     const size_t row = (size_t)(rq.q0 + j) * p.hq + (size_t)g * p.group + hh;
-    const float inv = 1.f / st.l;
+    const float inv = 1.f / l;
     uint16_t *o = p.out + row * D + 16 * e_lo + 4 * kq;
 #pragma unroll
     for (int u = 0; u < D / 16; ++u) {
@@ -374,7 +361,7 @@ __device__ __forceinline__ void write_tile(const AttnParams &p, int g, bool comp
       if (u >= ne) break;
       *reinterpret_cast<f32x4 *>(o + 16 * u) = st.o[u];
     }
-    if (kq == 0 && e_lo == 0) p.part_ml[prow] = make_float2(st.m, st.l);
+    if (kq == 0 && e_lo == 0) p.part_ml[prow] = make_float2(st.m, l);
   }
 }
 
@@ -456,81 +443,64 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
   return sh;
 }
 
-// Page id of page k (uniform, k < 128) of the current sub-piece, held one per
-// lane in two registers; -1 past the sub-piece.
-__device__ __forceinline__ int sub_page(int lo, int hi, int k, int npg) {
-  if (k >= npg) return -1;
-  return k < kWave ? __builtin_amdgcn_readlane(lo, k) : __builtin_amdgcn_readlane(hi, k - kWave);
-}
+// Everything a wave needs to run the ring over one sub-piece.
+template <int D>
+struct RingCtx {
+  const char *ring;      // LDS ring base
+  const int *pg;         // LDS page ids of the sub-piece (sanitised)
+  const char *kvw;       // this wave's tile of page 0: kv + (kind*Hkv + g) tiles
+  size_t page_bytes;     // bytes per page (2 * Hkv tiles)
+  uint32_t dst0;         // LDS byte address of this wave's DMA region in stage 0
+  uint32_t voff;         // this lane's swizzled global offset inside a chunk
+  int pp;                // page parity this wave loads
+  RingLane rl;
+  uint32_t vb;           // V operand offset of the wave's first d block
+  int nblk;              // blocks in the sub-piece
+  int sb, se, ctx, row_limit;
+  bool active;
+};
 
-// One pipeline step: wait for block b, load block b + kStages - 1 into the
-// stage block b - 1 used, compute block b.  The ring stages are separate LDS
-// arrays and the block loop is unrolled by the stage count, so every ring
-// load names a fixed array.
-template <int D, int NE>
-__device__ __forceinline__ void ring_step(const AttnParams &p, const uint4 (*cur)[kWave],
-                                          uint4 (*nxt)[kWave], int g, int b, int nblk, int npg,
-                                          int pid_lo, int pid_hi, int wave, int lane,
-                                          bool active, int sb, int se, int ctx, int row_limit,
-                                          const bf16x8 (&qv)[D / 32], int e_lo,
-                                          RowState<D> &st) {
-  using R = RingShape<D>;
+// One pipeline step with block b in compile-time stage ST: wait for block b,
+// load block b + kStages - 1 into the stage block b - 1 used, compute block b.
+template <int D, int NE, int ST>
+__device__ __forceinline__ void ring_step(const RingCtx<D> &c, int b, const bf16x8 (&qv)[D / 32],
+                                          float scale_log2, int lane, RowState<D> &st) {
+  using R = Ring<D>;
   // this wave's loads of block b are done once at most the loads of the
   // kStages-2 later blocks are outstanding; the barrier makes every wave's
   // part visible and frees the stage that block b-1 used
-  __builtin_amdgcn_s_waitcnt(waitcnt_imm((kStages - 2) * R::kOpsPerWave, 0));
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm((kStages - 2) * R::kChunks, 0));
   wg_barrier();
-  const int bn = min(b + kStages - 1, nblk - 1);  // clamped: extra loads land unread
-  ring_load<D>(p, g, sub_page(pid_lo, pid_hi, 2 * bn, npg),
-               sub_page(pid_lo, pid_hi, 2 * bn + 1, npg), nxt, wave, lane);
-  if (active) {
-    const int c0 = sub_page(pid_lo, pid_hi, 2 * b, npg);
-    const int c1 = sub_page(pid_lo, pid_hi, 2 * b + 1, npg);
-    const bool ok0 = (unsigned)c0 < (unsigned)p.num_pages;
-    const bool ok1 = (unsigned)c1 < (unsigned)p.num_pages;
-    const int t0 = sb + b * kBlockKeys;
-    const bool full = ok0 && ok1 && t0 + kBlockKeys <= min(ctx, se);
-    ring_compute<D, NE>(cur, lane, t0, se, row_limit, full, ok0, ok1, qv, e_lo, p.scale_log2,
-                        st);
+  const int bn = min(b + kStages - 1, c.nblk - 1);  // clamped: extra loads land unread
+  const int pid = __builtin_amdgcn_readfirstlane(c.pg[2 * bn + c.pp]);
+  ring_dma<D>(c.dst0 + ((ST + kStages - 1) % kStages) * R::kStage, c.voff,
+              c.kvw + (size_t)pid * c.page_bytes);
+  if (c.active) {
+    const int t0 = c.sb + b * kBlockKeys;
+    const bool full = t0 + kBlockKeys <= min(c.ctx, c.se);
+    ring_compute<D, NE>(c.ring, ST * R::kStage, c.rl, c.vb, lane, t0, c.se, c.row_limit, full,
+                        qv, scale_log2, st);
   }
 }
 
-// All blocks of one sub-piece (at most kSubPages pages) through the ring.
+// All blocks of one sub-piece through the ring.
 template <int D, int NE>
-__device__ __forceinline__ void ring_run(const AttnParams &p, uint4 (*r0)[kWave],
-                                         uint4 (*r1)[kWave], uint4 (*r2)[kWave],
-                                         uint4 (*r3)[kWave], int i, int g, int wave, int lane,
-                                         bool active, int sb, int se, int ctx, int row_limit,
-                                         const bf16x8 (&qv)[D / 32], int e_lo, RowState<D> &st) {
+__device__ __forceinline__ void ring_run(const RingCtx<D> &c, const bf16x8 (&qv)[D / 32],
+                                         float scale_log2, int lane, RowState<D> &st) {
+  using R = Ring<D>;
   static_assert(kStages == 4, "the block loop below is unrolled for four stages");
-  const int npg = (se - sb + kPage - 1) / kPage;
-  const int nblk = (se - sb + kBlockKeys - 1) / kBlockKeys;
-  // this sub-piece's page ids, one per lane in two registers
-  const int *pt = p.page_table + (size_t)i * p.max_pages + sb / kPage;
-  const int pid_lo = lane < npg ? pt[lane] : -1;
-  const int pid_hi = kWave + lane < npg ? pt[kWave + lane] : -1;
   // prologue: the first kStages-1 blocks
-  ring_load<D>(p, g, sub_page(pid_lo, pid_hi, 0, npg), sub_page(pid_lo, pid_hi, 1, npg), r0,
-               wave, lane);
-  {
-    const int b1 = min(1, nblk - 1), b2 = min(2, nblk - 1);
-    ring_load<D>(p, g, sub_page(pid_lo, pid_hi, 2 * b1, npg),
-                 sub_page(pid_lo, pid_hi, 2 * b1 + 1, npg), r1, wave, lane);
-    ring_load<D>(p, g, sub_page(pid_lo, pid_hi, 2 * b2, npg),
-                 sub_page(pid_lo, pid_hi, 2 * b2 + 1, npg), r2, wave, lane);
+#pragma unroll
+  for (int b = 0; b < kStages - 1; ++b) {
+    const int bb = min(b, c.nblk - 1);
+    const int pid = __builtin_amdgcn_readfirstlane(c.pg[2 * bb + c.pp]);
+    ring_dma<D>(c.dst0 + b * R::kStage, c.voff, c.kvw + (size_t)pid * c.page_bytes);
   }
-  for (int b = 0; b < nblk; b += kStages) {
-    ring_step<D, NE>(p, r0, r3, g, b, nblk, npg, pid_lo, pid_hi, wave, lane, active, sb, se,
-                     ctx, row_limit, qv, e_lo, st);
-    if (b + 1 < nblk)
-      ring_step<D, NE>(p, r1, r0, g, b + 1, nblk, npg, pid_lo, pid_hi, wave, lane, active, sb,
-                       se, ctx, row_limit, qv, e_lo, st);
-    if (b + 2 < nblk)
-      ring_step<D, NE>(p, r2, r1, g, b + 2, nblk, npg, pid_lo, pid_hi, wave, lane, active, sb,
-                       se, ctx, row_limit, qv, e_lo, st);
-    if (b + 3 < nblk)
-      ring_step<D, NE>(p, r3, r2, g, b + 3, nblk, npg, pid_lo, pid_hi, wave, lane, active, sb,
-                       se, ctx, row_limit, qv, e_lo, st);
+  for (int b = 0; b < c.nblk; b += kStages) {
+    ring_step<D, NE, 0>(c, b, qv, scale_log2, lane, st);
+    if (b + 1 < c.nblk) ring_step<D, NE, 1>(c, b + 1, qv, scale_log2, lane, st);
+    if (b + 2 < c.nblk) ring_step<D, NE, 2>(c, b + 2, qv, scale_log2, lane, st);
+    if (b + 3 < c.nblk) ring_step<D, NE, 3>(c, b + 3, qv, scale_log2, lane, st);
   }
   __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
   wg_barrier();  // the ring is free for the next sub-piece
@@ -538,11 +508,9 @@ __device__ __forceinline__ void ring_run(const AttnParams &p, uint4 (*r0)[kWave]
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p) {
-  using R = RingShape<D>;
-  __shared__ uint4 ring0[R::kOps][kWave];
-  __shared__ uint4 ring1[R::kOps][kWave];
-  __shared__ uint4 ring2[R::kOps][kWave];
-  __shared__ uint4 ring3[R::kOps][kWave];
+  using R = Ring<D>;
+  __shared__ __attribute__((aligned(1024))) char ring[kStages * R::kStage];
+  __shared__ int pg[kSubPages + 8];
   __shared__ int lds_plan[kWaves + 4];
 
   const Share sh = plan_share(p, lds_plan);
@@ -550,6 +518,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
   const int kq = lane >> 4, n = lane & 15;
+
+  // this wave's share of every ring load: page parity pp, K (waves 0-1) or V
+  const int pp = wave & 1, kind = wave >> 1;
+  RingCtx<D> c;
+  c.ring = ring;
+  c.pg = pg;
+  c.pp = pp;
+  c.page_bytes = (size_t)2 * p.hkv * kPage * D * sizeof(uint16_t);
+  c.dst0 = (uint32_t)(uintptr_t)ring + kind * R::kKRegion + pp * R::kChunks * 1024;
+  c.voff = 16u * (uint32_t)(kind == 0 ? k_unit(lane, pp) : v_unit_inv(lane));
+  c.rl = ring_lane<D>(lane);
 
   int i = sh.i, g = sh.g, off = sh.off, pos = sh.start, piece = 0;
   while (pos < sh.end && i < p.num_reqs) {
@@ -562,6 +541,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
     const int key_begin = off, key_end = min(rq.len, off + take);
     const bool complete = off == 0 && take == rq.seg;
     const int slot = piece == 0 ? 0 : 1;
+    c.kvw = reinterpret_cast<const char *>(p.kv) +
+            (size_t)(kind * p.hkv + g) * kPage * D * sizeof(uint16_t);
+    c.ctx = rq.ctx;
 
     // Wave roles.  Every wave computes every block of the piece:
     //  1 row tile:  all four waves on it, each with a quarter of the dims;
@@ -575,48 +557,61 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
     for (int pass = 0; pass < npass; ++pass) {
       const int rt = nds > 1 ? wave % nt : wave + kWaves * pass;
       const int ds = nds > 1 ? wave / nt : 0;
-      const bool active = rt < nt;
+      c.active = rt < nt;
       const int e_lo = ds * ne;
+      c.vb = c.rl.v + 512u * (uint32_t)e_lo;
       const int rr = rt * 16 + n;
-      const bool valid_row = active && rr < rows;
+      const bool valid_row = c.active && rr < rows;
       const int lg = __builtin_ctz(p.group);
       const int j = rr >> lg, hh = rr & (p.group - 1);
-      const int row_limit = valid_row ? rq.ctx + j : -1;
+      c.row_limit = valid_row ? rq.ctx + j : -1;
       bf16x8 qv[D / 32];
       {
         const uint16_t *qrow =
             p.q + ((size_t)(rq.q0 + j) * p.hq + (size_t)g * p.group + hh) * D;
 #pragma unroll
-        for (int c = 0; c < D / 32; ++c) {
+        for (int cc = 0; cc < D / 32; ++cc) {
           uint4 x = make_uint4(0, 0, 0, 0);
-          if (valid_row) x = *reinterpret_cast<const uint4 *>(qrow + 32 * c + 8 * kq);
-          qv[c] = as_bf16x8(x);
+          if (valid_row) x = *reinterpret_cast<const uint4 *>(qrow + 32 * cc + 8 * kq);
+          qv[cc] = as_bf16x8(x);
         }
+        // Make q resident here: the compiler does not see the ring loads,
+        // and a q load still pending at the block loop would otherwise make
+        // it wait for every load in flight inside the loop.
+#pragma unroll
+        for (int cc = 0; cc < D / 32; ++cc) asm volatile("" ::"v"(qv[cc]));
       }
       RowState<D> st;
       st.m = -INFINITY;
-      st.l = 0.f;
+      st.lacc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int e = 0; e < D / 16; ++e) st.o[e] = f32x4{0.f, 0.f, 0.f, 0.f};
 
       for (int sb = key_begin; sb < key_end; sb += kSubPages * kPage) {
         const int se = min(key_end, sb + kSubPages * kPage);
+        c.sb = sb;
+        c.se = se;
+        c.nblk = (se - sb + kBlockKeys - 1) / kBlockKeys;
+        // stage the sub-piece's page ids; an id outside [0, num_pages) breaks
+        // the contract and reads page 0 instead (valid memory, result
+        // unspecified), pages past the sub-piece read page 0 and are masked
+        {
+          const int npg = (se - sb + kPage - 1) / kPage;
+          const int *pt = p.page_table + (size_t)i * p.max_pages + sb / kPage;
+          for (int t = threadIdx.x; t < 2 * c.nblk; t += kThreads) {
+            int id = t < npg ? pt[t] : 0;
+            pg[t] = (unsigned)id < (unsigned)p.num_pages ? id : 0;
+          }
+          __syncthreads();
+        }
         if (ne == D / 16)
-          ring_run<D, D / 16>(p, ring0, ring1, ring2, ring3, i, g, wave, lane, active, sb, se,
-                              rq.ctx, row_limit, qv, e_lo, st);
+          ring_run<D, D / 16>(c, qv, p.scale_log2, lane, st);
         else if (ne == D / 32)
-          ring_run<D, D / 32>(p, ring0, ring1, ring2, ring3, i, g, wave, lane, active, sb, se,
-                              rq.ctx, row_limit, qv, e_lo, st);
+          ring_run<D, D / 32>(c, qv, p.scale_log2, lane, st);
         else
-          ring_run<D, D / 64>(p, ring0, ring1, ring2, ring3, i, g, wave, lane, active, sb, se,
-                              rq.ctx, row_limit, qv, e_lo, st);
+          ring_run<D, D / 64>(c, qv, p.scale_log2, lane, st);
       }
-      if (active) {
-        // the lane holds a partial row sum over its own keys; complete it
-        st.l += shfl_xor_f(st.l, 16);
-        st.l += shfl_xor_f(st.l, 32);
-        write_tile<D>(p, g, complete, slot, rq, rt, e_lo, ne, lane, st);
-      }
+      if (c.active) write_tile<D>(p, g, complete, slot, rq, rt, e_lo, ne, lane, st.lacc[0], st);
     }
 
     pos += take;
