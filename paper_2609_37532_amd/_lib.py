@@ -137,10 +137,11 @@ def accept_workspace_bytes(capacity: int, num_reqs: int, vocab: int) -> int:
 
 
 def alloc_workspace(nbytes: int, device=None):
-    """A 256-byte aligned uint8 device buffer of at least ``nbytes``."""
+    """A zero-filled, 256-byte aligned uint8 device buffer of at least ``nbytes``
+    (workspaces start zeroed once; the kernels leave them reusable)."""
     import torch
     dev = device if device is not None else torch.device("cuda", torch.cuda.current_device())
-    buf = torch.empty(max(1, nbytes) + 256, dtype=torch.uint8, device=dev)
+    buf = torch.zeros(max(1, nbytes) + 256, dtype=torch.uint8, device=dev)
     off = (-buf.data_ptr()) % 256
     return buf[off:off + max(1, nbytes)]
 

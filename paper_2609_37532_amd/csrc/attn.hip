@@ -675,32 +675,54 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
   };
 
   float mx = -INFINITY;
-  for (int u0 = 0; u0 < n_parts; u0 += 8) {
-    float m8[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      m8[u] = u0 + u < n_parts ? p.part_ml[prow(u0 + u)].x : -INFINITY;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) mx = fmaxf(mx, m8[u]);
-  }
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float den = 0.f;
-  for (int u0 = 0; u0 < n_parts; u0 += 8) {
+  if (n_parts <= 8) {
+    // the common case: every load in one round trip
     float2 l8[8];
     f32x4 o8[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const bool in = u0 + u < n_parts;
-      const size_t pr = prow(u0 + u);
+      const bool in = u < n_parts;
+      const size_t pr = prow(u);
       l8[u] = in ? p.part_ml[pr] : make_float2(-INFINITY, 0.f);
       o8[u] = in ? *reinterpret_cast<const f32x4 *>(p.part_o + pr * D + 4 * d4)
                  : f32x4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
+    for (int u = 0; u < 8; ++u) mx = fmaxf(mx, l8[u].x);
+#pragma unroll
     for (int u = 0; u < 8; ++u) {
       const float w = exp2f(l8[u].x - mx);
       den += w * l8[u].y;
       acc += w * o8[u];
+    }
+  } else {
+    for (int u0 = 0; u0 < n_parts; u0 += 8) {
+      float m8[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        m8[u] = u0 + u < n_parts ? p.part_ml[prow(u0 + u)].x : -INFINITY;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) mx = fmaxf(mx, m8[u]);
+    }
+    for (int u0 = 0; u0 < n_parts; u0 += 8) {
+      float2 l8[8];
+      f32x4 o8[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const bool in = u0 + u < n_parts;
+        const size_t pr = prow(u0 + u);
+        l8[u] = in ? p.part_ml[pr] : make_float2(-INFINITY, 0.f);
+        o8[u] = in ? *reinterpret_cast<const f32x4 *>(p.part_o + pr * D + 4 * d4)
+                   : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float w = exp2f(l8[u].x - mx);
+        den += w * l8[u].y;
+        acc += w * o8[u];
+      }
     }
   }
   const float inv = 1.f / den;
