@@ -23,11 +23,12 @@
 //    per workgroup.  Results depend only on the request's own data and the
 //    batch's total work (the share size), and merge in a fixed order, so
 //    they are deterministic.
-//  * K/V stream through an LDS ring of four 32-key blocks filled by
-//    LDS-direct loads three blocks ahead; each wave loads one 4 KiB tile
-//    per block (one page's K or V) as four contiguous 1 KiB loads from a
-//    scalar page address, so the loop spends almost no vector or scalar
-//    instructions on addressing.  Page ids are staged in LDS per piece.
+//  * K/V stream through an LDS ring of three 32-key blocks.  Each wave
+//    loads one 4 KiB tile per block (one page's K or V) into registers
+//    three blocks ahead, as four contiguous 1 KiB loads from a scalar page
+//    address, and writes it to the ring when its block comes up; on gfx950
+//    this sustains more bandwidth than LDS-direct loads.  Page ids are
+//    staged in LDS per piece.
 //  * Transposed scores: S^T = K Q^T and O^T = V^T P^T with
 //    v_mfma_f32_16x16x32_bf16.  The score tile comes out with one query row
 //    per lane column, which is exactly the B-operand layout the PV product
@@ -99,14 +100,13 @@ __device__ __forceinline__ ReqMeta load_req(const AttnParams &p, int i) {
 
 // ------------------------------------------------------------------ LDS ring
 // One 32-key block (two pages) in LDS: the K tiles of both pages, then their
-// V tiles, each tile as D/32 chunks of 1 KiB.  A wave fills one tile per
-// block with D/32 LDS-direct loads (global_load_lds_dwordx4): page
-// wave & 1, K for waves 0-1 and V for waves 2-3.  Each load reads one
-// contiguous KiB of the tile; lane l writes the 16 bytes at offset 16*l of
-// the chunk and fetches a swizzled 16-byte unit of it (each aligned group of
-// four lanes still fetches one aligned 64-byte piece), chosen so that the
-// MFMA operand reads are free of LDS bank conflicts for any grouping of 8,
-// 16 or 32 lanes per LDS cycle (k_unit / v_unit below).
+// V tiles, each tile as D/32 chunks of 1 KiB.  Wave w stages page w & 1's K
+// (waves 0-1) or V (waves 2-3) tile of every block.  Lane l writes the 16
+// bytes at offset 16*l of each chunk and loads a swizzled 16-byte unit of
+// it (each aligned group of four lanes still reads one aligned 64-byte
+// piece), chosen so that the MFMA operand reads are free of LDS bank
+// conflicts for any grouping of 8, 16 or 32 lanes per LDS cycle (k_unit /
+// v_unit below).
 template <int D>
 struct Ring {
   static constexpr int kChunks = D / 32;               // 1 KiB chunks per tile
@@ -114,49 +114,29 @@ struct Ring {
   static constexpr int kStage = 2 * kKRegion;          // 16 KiB at D = 128
   static constexpr int kKOps = 2 * kChunks;            // K operand tiles per block
 };
-constexpr int kStages = 4;      // blocks resident in the ring (3 in flight)
+constexpr int kStages = 3;      // ring stages = blocks in flight in registers
 constexpr int kSubPages = 512;  // page ids staged in LDS at a time (8192 keys)
 
-// s_waitcnt immediate (gfx9 encoding): wait until at most `vm` vector-memory
-// and `lgkm` LDS/scalar operations of this wave are outstanding.
-constexpr int waitcnt_imm(int vm, int lgkm) {
-  return (vm & 15) | (7 << 4) | ((lgkm & 15) << 8) | (((vm >> 4) & 3) << 14);
-}
-
-// Workgroup barrier without the memory fence __syncthreads() adds (that
-// fence would drain every ring load in flight); callers wait explicitly for
-// what must be complete first.
-__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-// The wave's LDS-direct loads of one block: the D/32 chunks of one tile at
-// `src` (uniform) into LDS at byte address `dst` (uniform).  The immediate
-// offset applies to both the global and the LDS address.  In asm so that
-// the compiler, which cannot tell ring stages apart, does not make its own
-// LDS reads wait for every ring load in flight; the explicit waits in
-// ring_step order them instead.
+// The wave's share of one block: one page's K or V tile (D/32 chunks of
+// 1 KiB), loaded into registers (lane l holds the swizzled unit it will
+// write at offset 16*l of each chunk) and later written to its ring stage.
 template <int D>
-__device__ __forceinline__ void ring_dma(uint32_t dst, uint32_t voff, const void *src);
+struct StageRegs {
+  u32x4 x[D / 32];
+};
 
-template <>
-__device__ __forceinline__ void ring_dma<128>(uint32_t dst, uint32_t voff, const void *src) {
-  asm volatile(
-      "s_mov_b32 m0, %0\n\t"
-      "global_load_lds_dwordx4 %1, %2 offset:0\n\t"
-      "global_load_lds_dwordx4 %1, %2 offset:1024\n\t"
-      "global_load_lds_dwordx4 %1, %2 offset:2048\n\t"
-      "global_load_lds_dwordx4 %1, %2 offset:3072" ::"s"(dst),
-      "v"(voff), "s"(src)
-      : "memory", "m0");
+template <int D>
+__device__ __forceinline__ void stage_load(const char *tile, uint32_t voff, StageRegs<D> &r) {
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c)
+    r.x[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(tile + voff + 1024 * c));
 }
 
-template <>
-__device__ __forceinline__ void ring_dma<64>(uint32_t dst, uint32_t voff, const void *src) {
-  asm volatile(
-      "s_mov_b32 m0, %0\n\t"
-      "global_load_lds_dwordx4 %1, %2 offset:0\n\t"
-      "global_load_lds_dwordx4 %1, %2 offset:1024" ::"s"(dst),
-      "v"(voff), "s"(src)
-      : "memory", "m0");
+template <int D>
+__device__ __forceinline__ void stage_store(char *dst, int lane, const StageRegs<D> &r) {
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c)
+    *reinterpret_cast<u32x4 *>(dst + 1024 * c + 16 * lane) = r.x[c];
 }
 
 // Key order inside a block.  Row m of score half hh holds key
@@ -450,7 +430,7 @@ struct RingCtx {
   const int *pg;         // LDS page ids of the sub-piece (sanitised)
   const char *kvw;       // this wave's tile of page 0: kv + (kind*Hkv + g) tiles
   size_t page_bytes;     // bytes per page (2 * Hkv tiles)
-  uint32_t dst0;         // LDS byte address of this wave's DMA region in stage 0
+  uint32_t dst0;         // byte offset of this wave's tile region in a stage
   uint32_t voff;         // this lane's swizzled global offset inside a chunk
   int pp;                // page parity this wave loads
   RingLane rl;
@@ -460,21 +440,28 @@ struct RingCtx {
   bool active;
 };
 
-// One pipeline step with block b in compile-time stage ST: wait for block b,
-// load block b + kStages - 1 into the stage block b - 1 used, compute block b.
+// Address of this wave's tile of block b (clamped: past the end it reloads
+// the last block, which is never read).
+template <int D>
+__device__ __forceinline__ const char *tile_of(const RingCtx<D> &c, int b) {
+  const int bb = min(b, c.nblk - 1);
+  const int pid = __builtin_amdgcn_readfirstlane(c.pg[2 * bb + c.pp]);
+  return c.kvw + (size_t)pid * c.page_bytes;
+}
+
+// One pipeline step with block b in compile-time stage ST: write the wave's
+// tile of block b (in registers since three steps ago) to the stage, start
+// loading block b + kStages into those registers, and after the barrier
+// compute block b.  The stage was last read at step b - kStages, which every
+// wave finished before the barrier of step b - kStages + 1.
 template <int D, int NE, int ST>
-__device__ __forceinline__ void ring_step(const RingCtx<D> &c, int b, const bf16x8 (&qv)[D / 32],
+__device__ __forceinline__ void ring_step(const RingCtx<D> &c, char *ring, int b,
+                                          StageRegs<D> &regs, const bf16x8 (&qv)[D / 32],
                                           float scale_log2, int lane, RowState<D> &st) {
   using R = Ring<D>;
-  // this wave's loads of block b are done once at most the loads of the
-  // kStages-2 later blocks are outstanding; the barrier makes every wave's
-  // part visible and frees the stage that block b-1 used
-  __builtin_amdgcn_s_waitcnt(waitcnt_imm((kStages - 2) * R::kChunks, 0));
-  wg_barrier();
-  const int bn = min(b + kStages - 1, c.nblk - 1);  // clamped: extra loads land unread
-  const int pid = __builtin_amdgcn_readfirstlane(c.pg[2 * bn + c.pp]);
-  ring_dma<D>(c.dst0 + ((ST + kStages - 1) % kStages) * R::kStage, c.voff,
-              c.kvw + (size_t)pid * c.page_bytes);
+  stage_store<D>(ring + ST * R::kStage + c.dst0, lane, regs);
+  stage_load<D>(tile_of<D>(c, b + kStages), c.voff, regs);
+  __syncthreads();
   if (c.active) {
     const int t0 = c.sb + b * kBlockKeys;
     const bool full = t0 + kBlockKeys <= min(c.ctx, c.se);
@@ -485,25 +472,31 @@ __device__ __forceinline__ void ring_step(const RingCtx<D> &c, int b, const bf16
 
 // All blocks of one sub-piece through the ring.
 template <int D, int NE>
-__device__ __forceinline__ void ring_run(const RingCtx<D> &c, const bf16x8 (&qv)[D / 32],
-                                         float scale_log2, int lane, RowState<D> &st) {
-  using R = Ring<D>;
-  static_assert(kStages == 4, "the block loop below is unrolled for four stages");
-  // prologue: the first kStages-1 blocks
-#pragma unroll
-  for (int b = 0; b < kStages - 1; ++b) {
-    const int bb = min(b, c.nblk - 1);
-    const int pid = __builtin_amdgcn_readfirstlane(c.pg[2 * bb + c.pp]);
-    ring_dma<D>(c.dst0 + b * R::kStage, c.voff, c.kvw + (size_t)pid * c.page_bytes);
+__device__ __forceinline__ void ring_run(const RingCtx<D> &c, char *ring,
+                                         const bf16x8 (&qv)[D / 32], float scale_log2, int lane,
+                                         RowState<D> &st) {
+  static_assert(kStages == 3, "the block loop below is unrolled for three stages");
+  // issued in block order (the empty asm keeps the compiler from reordering
+  // them), so that each step waits only for its own block
+  StageRegs<D> r0, r1, r2;
+  stage_load<D>(tile_of<D>(c, 0), c.voff, r0);
+  asm volatile("" ::: "memory");
+  stage_load<D>(tile_of<D>(c, 1), c.voff, r1);
+  asm volatile("" ::: "memory");
+  stage_load<D>(tile_of<D>(c, 2), c.voff, r2);
+  asm volatile("" ::: "memory");
+  // the loop leaves only through the breaks, so every path back to its head
+  // has issued the same loads in the same order and the compiler can wait
+  // for exactly the block each step writes
+  for (int b = 0;; b += kStages) {
+    ring_step<D, NE, 0>(c, ring, b, r0, qv, scale_log2, lane, st);
+    if (b + 1 >= c.nblk) break;
+    ring_step<D, NE, 1>(c, ring, b + 1, r1, qv, scale_log2, lane, st);
+    if (b + 2 >= c.nblk) break;
+    ring_step<D, NE, 2>(c, ring, b + 2, r2, qv, scale_log2, lane, st);
+    if (b + 3 >= c.nblk) break;
   }
-  for (int b = 0; b < c.nblk; b += kStages) {
-    ring_step<D, NE, 0>(c, b, qv, scale_log2, lane, st);
-    if (b + 1 < c.nblk) ring_step<D, NE, 1>(c, b + 1, qv, scale_log2, lane, st);
-    if (b + 2 < c.nblk) ring_step<D, NE, 2>(c, b + 2, qv, scale_log2, lane, st);
-    if (b + 3 < c.nblk) ring_step<D, NE, 3>(c, b + 3, qv, scale_log2, lane, st);
-  }
-  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 0));
-  wg_barrier();  // the ring is free for the next sub-piece
+  __syncthreads();  // the ring is free for the next sub-piece
 }
 
 template <int D>
@@ -526,7 +519,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
   c.pg = pg;
   c.pp = pp;
   c.page_bytes = (size_t)2 * p.hkv * kPage * D * sizeof(uint16_t);
-  c.dst0 = (uint32_t)(uintptr_t)ring + kind * R::kKRegion + pp * R::kChunks * 1024;
+  c.dst0 = kind * R::kKRegion + pp * R::kChunks * 1024;
   c.voff = 16u * (uint32_t)(kind == 0 ? k_unit(lane, pp) : v_unit_inv(lane));
   c.rl = ring_lane<D>(lane);
 
@@ -575,11 +568,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
           if (valid_row) x = *reinterpret_cast<const uint4 *>(qrow + 32 * cc + 8 * kq);
           qv[cc] = as_bf16x8(x);
         }
-        // Make q resident here: the compiler does not see the ring loads,
-        // and a q load still pending at the block loop would otherwise make
-        // it wait for every load in flight inside the loop.
-#pragma unroll
-        for (int cc = 0; cc < D / 32; ++cc) asm volatile("" ::"v"(qv[cc]));
+
       }
       RowState<D> st;
       st.m = -INFINITY;
@@ -605,11 +594,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
           __syncthreads();
         }
         if (ne == D / 16)
-          ring_run<D, D / 16>(c, qv, p.scale_log2, lane, st);
+          ring_run<D, D / 16>(c, ring, qv, p.scale_log2, lane, st);
         else if (ne == D / 32)
-          ring_run<D, D / 32>(c, qv, p.scale_log2, lane, st);
+          ring_run<D, D / 32>(c, ring, qv, p.scale_log2, lane, st);
         else
-          ring_run<D, D / 64>(c, qv, p.scale_log2, lane, st);
+          ring_run<D, D / 64>(c, ring, qv, p.scale_log2, lane, st);
       }
       if (c.active) write_tile<D>(p, g, complete, slot, rq, rt, e_lo, ne, lane, st.lacc[0], st);
     }
