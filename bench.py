@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--eager-only", type=int, default=0, metavar="N",
                     help="only run N eager steps (no graph, no timing, no CPU "
                          "baseline): the program that hardware-counter passes profile")
+    ap.add_argument("--no-stress", action="store_true",
+                    help="skip the 36-layer graph-replay stress measurement")
+    ap.add_argument("--stress-steps", type=int, default=100)
     ap.add_argument("--copy-probe", action="store_true",
                     help="only copy a 1 GiB device buffer three times: the plain copy "
                          "of known size that scales the hardware byte counters")
@@ -134,6 +137,51 @@ def cpu_baseline(attn, acc, seconds):
                       "the same batch, %d packed rows): fp64 attention over each "
                       "request's keys + acceptance of its rows, %.1f s, single thread"
                       % (done_reqs, passes, len(subs), done_tokens, t_total)}
+
+
+def stress_bench(steps):
+    """The graph-replay stress run (36 layers, B=32, contexts growing from
+    U[512, 4096]): per step, input staging outside the graph, one replay of
+    the captured 36-layer verify + acceptance graph timed with HIP events on
+    its stream, then the acceptance read back and the contexts grown.  Also
+    checks every step's acceptance against the planted values."""
+    import torch
+
+    import workloads as W
+    from workloads.stress import StressRun
+
+    plan = W.StressPlan(steps=steps)
+    run = StressRun(plan)
+    st = plan.draw_step()
+    run.stage(st)
+    run.capture()
+    times, tokens, kv_bytes, exact = [], 0, 0, True
+    hq, hkv, d = run.hq, run.hkv, run.d
+    for step in range(steps):
+        if step > 0:
+            st = plan.draw_step()
+            run.stage(st)
+        keys = (run.ctx_host + st.qlens)[st.qlens > 0]
+        kv_bytes += int(keys.sum()) * hkv * d * 2 * 2 * plan.num_layers
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(run.stream)
+        run.replay()
+        e1.record(run.stream)
+        a, nxt = run.finish(st)
+        exact &= bool((a == st.planted_accept_len).all() and (nxt == st.planted_next).all())
+        times.append(e0.elapsed_time(e1))
+        tokens += int(st.qlens.sum())
+    run.close()
+    total_ms = float(np.sum(times))
+    return {"workload": "36 layers (36 KV pools) of Qwen3-8B-shape verify attention + acceptance "
+                        "over 151936 tokens, B=32, contexts from U[512,4096] growing by "
+                        "accepted+1 per step, one hipGraph replay per step",
+            "steps": steps, "ms_per_step": round(total_ms / steps, 4),
+            "us_per_layer_incl_accept": round(total_ms / steps * 1e3 / plan.num_layers, 2),
+            "packed_tokens_per_s": round(tokens / (total_ms * 1e-3), 1),
+            "kv_gbps": round(kv_bytes / (total_ms * 1e-3) / 1e9, 1),
+            "acceptance_exact_every_step": exact}
 
 
 def copy_probe():
@@ -298,6 +346,11 @@ def main():
     }
     graph.close()
 
+    del q, kv, logits, out
+    torch.cuda.empty_cache()
+    if not args.no_stress:
+        log("stress run (36 layers, %d steps) ..." % args.stress_steps)
+        result["stress"] = stress_bench(args.stress_steps)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(attn, acc, args.cpu_seconds)

@@ -24,4 +24,6 @@ from .gen import (  # noqa: F401
     v_tile_offset,
     verify_lengths,
     CONFIGS,
+    StressPlan,
+    StressStep,
 )

@@ -406,3 +406,80 @@ def config_accept_inputs(index: int, cu_qlens, rng: np.random.Generator,
     return make_accept_inputs(rng, cu_qlens=cu_qlens, capacity=c["capacity"],
                               vocab=c["vocab"], dtype=c["accept_dtype"],
                               p_accept=c["p_accept"], poison=poison)
+
+
+# --------------------------------------------------------------------------
+# config 5: graph-replay stress (host side of the plan)
+# --------------------------------------------------------------------------
+CONFIGS[5] = dict(name="graph-replay stress", num_layers=36, num_reqs=32, num_q_heads=32,
+                  num_kv_heads=8, head_dim=128, capacity=256, ctx_range=(512, 4096),
+                  steps=100, vocab=151936, accept_dtype="bf16", p_accept=0.3)
+
+
+@dataclass
+class StressStep:
+    """One step's inputs: verify lengths, packed offsets, packed draft tokens,
+    and the planted acceptance (accepted count and successor per request)
+    with the (row, token) logits it boosts."""
+    qlens: np.ndarray
+    cu_qlens: np.ndarray
+    draft_tokens: np.ndarray
+    planted_accept_len: np.ndarray
+    planted_next: np.ndarray
+    boost_rows: np.ndarray
+    boost_tokens: np.ndarray
+
+
+class StressPlan:
+    """Seeded host plan of the stress run: initial contexts, one page table
+    (logical page -> physical page, a random permutation of the pool, shared
+    by every layer's pool) sized for the longest context the run can reach,
+    and per step the lengths, drafts and planted acceptances.  Contexts grow
+    by the accepted count plus one after every step."""
+
+    def __init__(self, steps: Optional[int] = None, num_layers: Optional[int] = None,
+                 num_reqs: Optional[int] = None, rng: Optional[np.random.Generator] = None):
+        c = CONFIGS[5]
+        self.rng = config_rng(5) if rng is None else rng
+        self.steps = c["steps"] if steps is None else steps
+        self.num_layers = c["num_layers"] if num_layers is None else num_layers
+        self.B = c["num_reqs"] if num_reqs is None else num_reqs
+        self.capacity = c["capacity"]
+        self.vocab = c["vocab"]
+        self.p_accept = c["p_accept"]
+        lo, hi = c["ctx_range"]
+        self.ctx0 = self.rng.integers(lo, hi + 1, size=self.B).astype(np.int32)
+        # the longest context: start + steps * (up to W per step) + one block
+        self.max_kv_len = int(hi + (self.steps + 1) * BLOCK_WIDTH)
+        self.max_pages = -(-self.max_kv_len // PAGE_SIZE)
+        self.num_pages = self.B * self.max_pages
+        self.page_table = self.rng.permutation(self.num_pages).astype(np.int32).reshape(
+            self.B, self.max_pages)
+
+    def draw_step(self) -> StressStep:
+        B, cap, V = self.B, self.capacity, self.vocab
+        k = verify_lengths(self.rng, B, cap, p=0.25)
+        cu = cu_from_lengths(k)
+        draft = self.rng.integers(0, V, size=cap, dtype=np.int64).astype(np.int32)
+        a = np.zeros(B, dtype=np.int32)
+        nxt = np.full(B, -1, dtype=np.int32)
+        rows, toks = [], []
+        for i in range(B):
+            o, kk = int(cu[i]), int(k[i])
+            if kk == 0:
+                continue
+            a[i] = min(int(self.rng.geometric(self.p_accept)) - 1, kk - 1)
+            for j in range(int(a[i])):
+                rows.append(o + j)
+                toks.append(int(draft[o + j + 1]))
+            if a[i] < kk - 1:
+                avoid = int(draft[o + a[i] + 1])
+                x = (avoid + 1 + int(self.rng.integers(0, V - 1))) % V
+            else:
+                x = int(self.rng.integers(0, V))
+            nxt[i] = x
+            rows.append(o + int(a[i]))
+            toks.append(x)
+        return StressStep(qlens=k, cu_qlens=cu, draft_tokens=draft, planted_accept_len=a,
+                          planted_next=nxt, boost_rows=np.asarray(rows, np.int64),
+                          boost_tokens=np.asarray(toks, np.int64))
