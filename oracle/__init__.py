@@ -127,3 +127,77 @@ def accept(logits, dtype, cu_qlens, draft_tokens):
     if rc != 0:
         raise ValueError("oracle_accept rejected its input (rc=%d)" % rc)
     return a, nxt
+
+
+# ---------------------------------------------------------------- DVL (Sec. III-C)
+def dvl_scores(pred_logits, w):
+    """Prefix scores, estimates and initial lengths (Alg. 1, Eqs. (6)-(7)).
+
+    ``pred_logits`` float32 [n, w-1]; returns ``(q [n, w] f32, ell [n] f32,
+    k0 [n] i32)``."""
+    lib = _load()
+    lg = _c(pred_logits, np.float32).reshape(-1, w - 1)
+    n = lg.shape[0]
+    q = np.zeros((n, w), np.float32)
+    ell = np.zeros(n, np.float32)
+    k0 = np.zeros(n, np.int32)
+    rc = lib.oracle_dvl_scores(_ptr(lg), n, w, _ptr(q), _ptr(ell), _ptr(k0))
+    if rc != 0:
+        raise ValueError("oracle_dvl_scores rejected its input (rc=%d)" % rc)
+    return q, ell, k0
+
+
+def dvl_adjust(q, k0, budget):
+    """Budget adjustment (Eqs. (8)-(9)); returns ``(k [n] i32, updates)``."""
+    lib = _load()
+    q = _c(q, np.float32)
+    n, w = q.shape
+    k0 = _c(k0, np.int32)
+    k = np.zeros(n, np.int32)
+    upd = ctypes.c_int32(0)
+    rc = lib.oracle_dvl_adjust(_ptr(q), _ptr(k0), n, w, int(budget), _ptr(k),
+                               ctypes.byref(upd))
+    if rc != 0:
+        raise ValueError("oracle_dvl_adjust rejected its input (rc=%d)" % rc)
+    return k, int(upd.value)
+
+
+def dvl_pack(k_live, n_bs, w, m_bs, tokens, positions, kv_refs):
+    """Offsets, packing, sentinels and tail placeholders (Eqs. (10)-(11)).
+
+    Fields are int32 [n_bs, w]; returns a dict with ``k`` [n_bs],
+    ``offsets`` [n_bs+1] and ``tokens``, ``positions``, ``kv_refs`` [m_bs]."""
+    lib = _load()
+    kl = _c(k_live, np.int32)
+    fields = [_c(f, np.int32).reshape(n_bs, w) for f in (tokens, positions, kv_refs)]
+    k = np.zeros(n_bs, np.int32)
+    off = np.zeros(n_bs + 1, np.int32)
+    packed = [np.zeros(m_bs, np.int32) for _ in range(3)]
+    rc = lib.oracle_dvl_pack(_ptr(kl), kl.shape[0], n_bs, w, m_bs, *[_ptr(f) for f in fields],
+                             _ptr(k), _ptr(off), *[_ptr(p) for p in packed])
+    if rc != 0:
+        raise ValueError("oracle_dvl_pack rejected its input (rc=%d)" % rc)
+    return dict(k=k, offsets=off, tokens=packed[0], positions=packed[1], kv_refs=packed[2])
+
+
+def dvl_allocate_pack(pred_logits, n_live, tokens, positions, kv_refs, w=16):
+    """Alg. 1 end to end for a bucket of ``n_bs`` requests of which the first
+    ``n_live`` are live: budget M_live = w*n_live/2, capacity M_bs = w*n_bs/2.
+
+    Returns the :func:`dvl_pack` dict plus ``q`` [n_bs, w] (zero rows for
+    sentinels), ``k0`` [n_live], ``ell`` [n_live] and ``updates``."""
+    lg = _c(pred_logits, np.float32).reshape(-1, w - 1)
+    n_bs = lg.shape[0]
+    n = int(n_live)
+    assert 0 <= n <= n_bs and w % 2 == 0
+    q = np.zeros((n_bs, w), np.float32)
+    if n > 0:
+        ql, ell, k0 = dvl_scores(lg[:n], w)
+        q[:n] = ql
+        k, upd = dvl_adjust(ql, k0, w * n // 2)
+    else:
+        ell, k0, k, upd = (np.zeros(0, np.float32), np.zeros(0, np.int32),
+                           np.zeros(0, np.int32), 0)
+    res = dvl_pack(k, n_bs, w, w * n_bs // 2, tokens, positions, kv_refs)
+    res.update(q=q, k0=k0, ell=ell, updates=upd)
+    return res

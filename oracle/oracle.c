@@ -4,8 +4,10 @@
  *
  * TEST INFRASTRUCTURE ONLY: only tests/, __graft_entry__.smoke() and the
  * CPU-baseline leg of bench.py load it.  It shares no code, header or table
- * with the HIP library.  Every floating-point step is in double precision;
- * bf16 and fp32 inputs widen to double exactly.
+ * with the HIP library.  Every floating-point step of attention and
+ * acceptance is in double precision (bf16 and fp32 inputs widen to double
+ * exactly); the DVL allocator takes its decisions on binary32 scores, in the
+ * precision the library decides in (oracle.h).
  *
  * What is computed (the method reaches these exactly, so the oracle is the
  * plain definition written out):
@@ -25,6 +27,10 @@
  *    target's argmax at the previous row, the first mismatch stops the
  *    prefix, and row offset_i + a_i supplies the successor.  Sec. I: the
  *    accepted tokens are the contiguous candidate prefix, anchor excluded.
+ *
+ *  - DVL budget allocation and flat-buffer packing.  Sec. III-C, Alg. 1 and
+ *    Eqs. (6)-(11): taken step by step in the paper's order (an iteration,
+ *    not a closed form); see the section at the end of this file.
  *
  * Input formats restated from the library's public contract: bf16 values
  * are the upper 16 bits of an IEEE binary32; a KV page holds, per KV head,
@@ -198,5 +204,123 @@ int oracle_accept(const void *logits, int32_t dtype, const int32_t *cu_qlens,
     next_token[i] = target[o + a];
   }
   free(target);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * DVL budget allocation and flat-buffer packing (Sec. III-C).
+ *
+ * Alg. 1 in the paper's order: sigmoid scores with the anchor's score fixed at
+ * one and a running minimum so that scores never increase along the block
+ * (Eq. (6)); the estimate is the sum of the W-1 draft scores, rounded half up
+ * and clipped to [1, W] (Eq. (7)); the gap to the budget is closed one slot
+ * at a time, growing the request whose next slot scores highest or shrinking
+ * the one whose last slot scores lowest (Eq. (9)); offsets are the exclusive
+ * prefix sum (Eq. (10)) and every field is copied to offset_i + j (Eq. (11));
+ * requests past the live count get length 0 and offset M_live, and slots past
+ * M_live get token 0, position 0 and the first request's first cache
+ * reference.
+ *
+ * Readings: the paper leaves the tie-break of Eq. (9) open; here the lowest
+ * request index wins.  It fixes no precision; decisions are taken on binary32
+ * scores (see oracle.h).  A NaN score leaves the running minimum unchanged.
+ * ---------------------------------------------------------------------- */
+
+int oracle_dvl_scores(const float *pred_logits, int32_t n, int32_t w,
+                      float *q, float *ell, int32_t *k0) {
+  if (n < 0 || w < 2 || w > 64 || (n > 0 && (!pred_logits || !q || !ell || !k0)))
+    return -1;
+  for (int32_t i = 0; i < n; ++i) {
+    float *qi = q + (int64_t)i * w;
+    qi[0] = 1.0f;
+    for (int32_t j = 1; j < w; ++j) {
+      double x = (double)pred_logits[(int64_t)i * (w - 1) + (j - 1)];
+      float sig = (float)(1.0 / (1.0 + exp(-x)));
+      qi[j] = (sig < qi[j - 1]) ? sig : qi[j - 1];
+    }
+    float sum = 0.0f;
+    for (int32_t j = 1; j < w; ++j) sum += qi[j];
+    ell[i] = sum;
+    float r = floorf(sum + 0.5f);
+    int32_t k = r < 1.0f ? 1 : (r > (float)w ? w : (int32_t)r);
+    k0[i] = k;
+  }
+  return 0;
+}
+
+int oracle_dvl_adjust(const float *q, const int32_t *k0, int32_t n, int32_t w,
+                      int32_t budget, int32_t *k, int32_t *updates) {
+  if (n < 1 || w < 2 || !q || !k0 || !k || !updates) return -1;
+  if (budget < n || (int64_t)budget > (int64_t)n * w) return -1;
+  int64_t sum = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (k0[i] < 1 || k0[i] > w) return -1;
+    k[i] = k0[i];
+    sum += k0[i];
+  }
+  int64_t gap = (int64_t)budget - sum;
+  int32_t count = 0;
+  while (gap > 0) {
+    int32_t best = -1;
+    for (int32_t i = 0; i < n; ++i) {
+      if (k[i] >= w) continue;
+      if (best < 0 || q[(int64_t)i * w + k[i]] > q[(int64_t)best * w + k[best]]) best = i;
+    }
+    if (best < 0) return -1; /* unreachable for a budget within [n, n*w] */
+    k[best] += 1;
+    gap -= 1;
+    ++count;
+  }
+  while (gap < 0) {
+    int32_t best = -1;
+    for (int32_t i = 0; i < n; ++i) {
+      if (k[i] <= 1) continue;
+      if (best < 0 || q[(int64_t)i * w + k[i] - 1] < q[(int64_t)best * w + k[best] - 1])
+        best = i;
+    }
+    if (best < 0) return -1;
+    k[best] -= 1;
+    gap += 1;
+    ++count;
+  }
+  *updates = count;
+  return 0;
+}
+
+int oracle_dvl_pack(const int32_t *k_live, int32_t n, int32_t n_bs, int32_t w,
+                    int32_t m_bs, const int32_t *tokens,
+                    const int32_t *positions, const int32_t *kv_refs,
+                    int32_t *k_out, int32_t *offsets, int32_t *packed_tokens,
+                    int32_t *packed_positions, int32_t *packed_kv_refs) {
+  if (n < 0 || n_bs < 1 || n > n_bs || w < 1 || m_bs < 0) return -1;
+  if (!tokens || !positions || !kv_refs || !k_out || !offsets) return -1;
+  if (m_bs > 0 && (!packed_tokens || !packed_positions || !packed_kv_refs)) return -1;
+  int64_t live = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (k_live[i] < 1 || k_live[i] > w) return -1;
+    live += k_live[i];
+  }
+  if (live > m_bs) return -1;
+  /* offsets of live requests, then sentinels: length 0 at offset M_live */
+  offsets[0] = 0;
+  for (int32_t i = 0; i < n_bs; ++i) {
+    k_out[i] = i < n ? k_live[i] : 0;
+    offsets[i + 1] = offsets[i] + k_out[i];
+  }
+  /* every live slot: the field value of (request, position) it maps to */
+  for (int32_t i = 0; i < n; ++i) {
+    for (int32_t j = 0; j < k_out[i]; ++j) {
+      int32_t s = offsets[i] + j;
+      packed_tokens[s] = tokens[(int64_t)i * w + j];
+      packed_positions[s] = positions[(int64_t)i * w + j];
+      packed_kv_refs[s] = kv_refs[(int64_t)i * w + j];
+    }
+  }
+  /* tail placeholders */
+  for (int64_t s = live; s < m_bs; ++s) {
+    packed_tokens[s] = 0;
+    packed_positions[s] = 0;
+    packed_kv_refs[s] = kv_refs[0];
+  }
   return 0;
 }

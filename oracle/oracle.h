@@ -33,4 +33,33 @@ int oracle_accept(const void *logits, int32_t dtype, const int32_t *cu_qlens,
                   int32_t *next_token, int32_t num_reqs, int32_t cap,
                   int32_t vocab);
 
+/* ---- DVL budget allocation and flat-buffer packing (Sec. III-C) ----
+ *
+ * Decisions are taken in single precision, as the library takes them: each
+ * prefix score is the binary32 rounding of the sigmoid evaluated in double,
+ * the cumulative minimum and all comparisons act on those binary32 values,
+ * and the length estimate is a binary32 sum in position order. */
+
+/* Prefix scores and initial lengths (Alg. 1 score and seed steps, Eqs. (6)
+ * and (7)).  pred_logits float [n][w-1]; writes q float [n][w] (q[i][0] = 1),
+ * ell float [n] (the estimate) and k0 [n].  2 <= w <= 64. */
+int oracle_dvl_scores(const float *pred_logits, int32_t n, int32_t w,
+                      float *q, float *ell, int32_t *k0);
+
+/* Budget adjustment (Eqs. (8) and (9), Alg. 1 grow and shrink loops): one
+ * request at a time, lowest request index on ties.  Requires 1 <= k0 <= w and
+ * n <= budget <= n*w.  Writes k [n] and the number of single-slot updates. */
+int oracle_dvl_adjust(const float *q, const int32_t *k0, int32_t n, int32_t w,
+                      int32_t budget, int32_t *k, int32_t *updates);
+
+/* Offsets, packing, sentinels and tail placeholders (Eqs. (10) and (11), Alg.
+ * 1 pack and sentinel steps).  k_live [n] (each in [1, w]); fields int32
+ * [n_bs][w]; writes k_out [n_bs], offsets [n_bs+1] and the three packed
+ * fields [m_bs].  Requires 0 <= n <= n_bs and sum(k_live) <= m_bs. */
+int oracle_dvl_pack(const int32_t *k_live, int32_t n, int32_t n_bs, int32_t w,
+                    int32_t m_bs, const int32_t *tokens,
+                    const int32_t *positions, const int32_t *kv_refs,
+                    int32_t *k_out, int32_t *offsets, int32_t *packed_tokens,
+                    int32_t *packed_positions, int32_t *packed_kv_refs);
+
 #endif

@@ -26,4 +26,6 @@ from .gen import (  # noqa: F401
     CONFIGS,
     StressPlan,
     StressStep,
+    DvlInputs,
+    make_dvl_inputs,
 )

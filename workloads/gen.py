@@ -483,3 +483,57 @@ class StressPlan:
         return StressStep(qlens=k, cu_qlens=cu, draft_tokens=draft, planted_accept_len=a,
                           planted_next=nxt, boost_rows=np.asarray(rows, np.int64),
                           boost_tokens=np.asarray(toks, np.int64))
+
+
+# --------------------------------------------------------------------- DVL
+@dataclass
+class DvlInputs:
+    """Inputs of the DVL allocator and packer for one bucket of ``n_bs``
+    request slots, the first ``n_live`` live.
+
+    ``pred_logits`` float32 [n_bs, W-1]: synthetic predictor outputs.  Each
+    live request draws a per-position acceptance rate r ~ U(rate_range)
+    (default U(0.85, 0.995), which puts the mean estimate near the W/2 budget
+    per request, so both growing and shrinking occur); its
+    logit at draft position j is log(r^j / (1 - r^j)) plus N(0, noise) noise
+    (default 0.5),
+    so the sigmoid profile decays like the geometric acceptance model with
+    some non-monotone noise for the running minimum to remove.  With
+    ``ties`` the logits are rounded to a 0.5 grid so that equal scores across
+    requests are common.  Sentinel rows hold NaN (never read).
+    ``tokens`` [n_bs, W]: the anchor plus W-1 drafts, uniform over the
+    vocabulary.  ``positions`` [n_bs, W]: ctx_i + j.  ``kv_refs`` [n_bs, W]:
+    flat cache slots (page * 16 + slot) of those positions under a random
+    page assignment."""
+    pred_logits: np.ndarray
+    n_live: int
+    tokens: np.ndarray
+    positions: np.ndarray
+    kv_refs: np.ndarray
+    width: int
+
+
+def make_dvl_inputs(rng: np.random.Generator, *, n_bs: int, n_live: int,
+                    width: int = BLOCK_WIDTH, vocab: int = 151936,
+                    ctx_range=(256, 4096), noise: float = 0.5,
+                    rate_range=(0.85, 0.995), ties: bool = False) -> DvlInputs:
+    if not (0 <= n_live <= n_bs):
+        raise ValueError("need 0 <= n_live <= n_bs")
+    w = width
+    rate = rng.uniform(rate_range[0], rate_range[1], size=(n_bs, 1))
+    j = np.arange(1, w, dtype=np.float64)[None, :]
+    p = np.clip(rate ** j, 1e-6, 1 - 1e-6)
+    logits = np.log(p / (1 - p)) + rng.normal(0.0, noise, size=(n_bs, w - 1))
+    if ties:
+        logits = np.round(logits * 2.0) / 2.0
+    logits = logits.astype(np.float32)
+    logits[n_live:] = np.nan
+    tokens = rng.integers(0, vocab, size=(n_bs, w), dtype=np.int64).astype(np.int32)
+    ctx = rng.integers(ctx_range[0], ctx_range[1] + 1, size=(n_bs, 1))
+    positions = (ctx + np.arange(w)[None, :]).astype(np.int32)
+    pages_per_req = -(-(ctx_range[1] + w) // PAGE_SIZE)
+    page_of = rng.permutation(n_bs * pages_per_req).reshape(n_bs, pages_per_req)
+    kv_refs = np.take_along_axis(page_of, positions // PAGE_SIZE, axis=1) * PAGE_SIZE \
+        + positions % PAGE_SIZE
+    return DvlInputs(pred_logits=logits, n_live=int(n_live), tokens=tokens,
+                     positions=positions, kv_refs=kv_refs.astype(np.int32), width=w)
