@@ -3,7 +3,8 @@
  * (DScale, "Scaling Block-Diffusion Speculative Decoding with Adaptive
  * Verification"), built for AMD Instinct MI355X (gfx950).
  *
- * The library exposes the two operations of the target-verification hot path:
+ * The library exposes the two operations of the target-verification hot path,
+ * and the decision step that produces its packed layout:
  *
  *   dsv_verify_attn  ragged, packed verify attention over a paged bf16 GQA KV
  *                    cache (Sec. III-B tile routing, Sec. III-D Eq. (16) row
@@ -11,7 +12,13 @@
  *   dsv_accept       greedy acceptance: per-row vocabulary argmax followed by
  *                    the longest-prefix compare against the drafted tokens
  *                    (Sec. III-D "Prefix verifier", greedy case; Sec. I
- *                    definition of accepted tokens).
+ *                    definition of accepted tokens);
+ *   dsv_dvl_allocate_pack
+ *                    DVL budget allocation and flat-buffer packing (Sec.
+ *                    III-C, Alg. 1, Eqs. (6)-(11)): per-request verify
+ *                    lengths under the shared budget, the offsets that
+ *                    dsv_verify_attn and dsv_accept read as cu_qlens, and the
+ *                    packed token, position and cache-reference rows.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -209,6 +216,62 @@ int dsv_validate_metadata(const int32_t *cu_qlens, const int32_t *ctx_lens,
                           int32_t *err_word, void *hip_stream);
 
 /*
+ * DVL budget allocation and flat-buffer packing (Sec. III-C, Alg. 1), for a
+ * captured bucket of N_bs request slots of which the first N are live
+ * (1 <= N <= N_bs; the rest are sentinels).  W = block_width (16 in the
+ * paper), M_live = W*N/2 live rows, M_bs = W*N_bs/2 rows of capacity (Eq. (3)).
+ *
+ *  1. Prefix scores (Eq. (6)): q_{i,0} = 1 and q_{i,j} = min(q_{i,j-1},
+ *     sigmoid(pred_logits[i][j-1])) for j = 1 .. W-1.
+ *  2. Initial lengths (Eq. (7)): the estimate is the sum of q_{i,1..W-1}; the
+ *     seed is that estimate plus one half, floored, clipped to [1, W].
+ *  3. Budget adjustment (Eqs. (8)-(9)): the gap M_live - sum(seeds) is closed
+ *     one slot at a time, growing the request whose next slot q_{i,k_i}
+ *     scores highest (k_i < W) or shrinking the one whose last slot
+ *     q_{i,k_i-1} scores lowest (k_i > 1).  Ties go to the lowest request
+ *     index (the paper leaves them open).  The result is the same as that
+ *     one-at-a-time loop, computed here without |gap| serial steps.
+ *  4. Offsets (Eq. (10)) and packing (Eq. (11)): row offset_i + j of each
+ *     packed field holds field_i[j] for j < k_i.  Sentinel requests get
+ *     k = 0 and offset M_live; rows M_live .. M_bs-1 get token 0, position 0
+ *     and the cache reference kv_refs[0][0].
+ *
+ * Precision: each score is the binary32 rounding of the sigmoid evaluated in
+ * double precision; the running minimum, the estimate (a binary32 sum in
+ * position order) and every comparison act on binary32 values.  The result
+ * is deterministic and independent of the launch.
+ *
+ * Arguments (device pointers unless stated):
+ *   pred_logits      fp32 [N_bs][W-1], predictor outputs (Eq. (5)); rows of
+ *                    sentinel slots are not read.  A NaN logit leaves the
+ *                    running minimum unchanged.
+ *   num_live         int32 scalar N, read on the device (so a captured graph
+ *                    can replay with another live count); values outside
+ *                    [0, N_bs] are clamped into it (N = 0 gives M_live = 0).
+ *   tokens, positions, kv_refs
+ *                    int32 [N_bs][W], each request's full drafted block
+ *                    (anchor first); only rows j < k_i of live requests and
+ *                    kv_refs[0][0] are read.
+ *   k_out            int32 [N_bs], written: lengths (0 for sentinels).
+ *   cu_qlens         int32 [N_bs+1], written: offsets, cu_qlens[N_bs] = M_live.
+ *   packed_tokens, packed_positions, packed_kv_refs
+ *                    int32 [M_bs] each, written in full.
+ *   scores_out       fp32 [N_bs][W] or NULL: the prefix scores (zero rows for
+ *                    sentinels).
+ *   bucket_reqs      N_bs, host value in [1, DSV_DVL_MAX_REQS].
+ *   block_width      W, host value, even, in [2, DSV_MAX_QLEN].
+ * One workgroup; no workspace; capturable like every other call.
+ */
+#define DSV_DVL_MAX_REQS 1024
+int dsv_dvl_allocate_pack(const float *pred_logits, const int32_t *num_live,
+                          const int32_t *tokens, const int32_t *positions,
+                          const int32_t *kv_refs, int32_t *k_out,
+                          int32_t *cu_qlens, int32_t *packed_tokens,
+                          int32_t *packed_positions, int32_t *packed_kv_refs,
+                          float *scores_out, int32_t bucket_reqs,
+                          int32_t block_width, void *hip_stream);
+
+/*
  * Graph helpers for the fixed-address replay of Alg. 2 (capture once, replay
  * each step) under the workspace invariant of Eq. (13): while a stream is
  * being captured, dsv_verify_attn / dsv_accept calls (and any other work
@@ -232,15 +295,16 @@ int dsv_graph_destroy(void *graph_exec);
 
 /*
  * Kernel timing for measurement harnesses.  After dsv_timing_start(n), the
- * next n kernel launches made by eager (not captured) dsv_verify_attn /
- * dsv_accept calls are bracketed by HIP events recorded on the caller's
- * stream.  dsv_timing_stop waits for those events, writes per kernel kind the
- * summed milliseconds and the launch count (arrays of DSV_TIMING_KINDS), and
- * turns timing off.  Kinds: 0 attention split kernel, 1 attention combine
- * kernel, 2 vocabulary argmax kernel, 3 prefix-compare kernel.  Not
- * thread-safe against concurrent calls from several host threads.
+ * next n kernel launches made by eager (not captured) dsv_verify_attn,
+ * dsv_accept and dsv_dvl_allocate_pack calls are bracketed by HIP events
+ * recorded on the caller's stream.  dsv_timing_stop waits for those events,
+ * writes per kernel kind the summed milliseconds and the launch count (arrays
+ * of DSV_TIMING_KINDS), and turns timing off.  Kinds: 0 attention split
+ * kernel, 1 attention combine kernel, 2 vocabulary argmax kernel,
+ * 3 prefix-compare kernel, 4 DVL allocate-and-pack kernel.  Not thread-safe
+ * against concurrent calls from several host threads.
  */
-#define DSV_TIMING_KINDS 4
+#define DSV_TIMING_KINDS 5
 int dsv_timing_start(int32_t max_launches);
 int dsv_timing_stop(float *total_ms, int32_t *launches);
 

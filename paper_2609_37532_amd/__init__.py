@@ -6,7 +6,12 @@ Two operations behind the C ABI of ``libdsv.so`` (declared in
 * ``verify_attn(q_packed, cu_qlens, kv_pages, page_table, ctx_lens, out)`` --
   ragged, packed verify attention over a paged bf16 GQA KV cache;
 * ``accept(logits_packed, cu_qlens, draft_tokens, accept_len, next_token)`` --
-  greedy acceptance (per-row vocabulary argmax + longest-prefix compare).
+  greedy acceptance (per-row vocabulary argmax + longest-prefix compare);
+
+and the decision step that produces their packed layout:
+
+* ``dvl_allocate_pack(...)`` -- DVL budget allocation and flat-buffer packing
+  (verify lengths under the shared budget, the offsets, the packed rows).
 
 This module only marshals arguments; PyTorch provides device memory and
 streams.  ``Graph`` captures and replays the calls with fixed buffer
@@ -14,6 +19,7 @@ addresses; ``KernelTimer`` times the kernels with HIP events.
 """
 from ._lib import (  # noqa: F401
     DSV_BF16,
+    DVL_MAX_REQS,
     DSV_F32,
     LIB_PATH,
     MAX_QLEN,
@@ -27,6 +33,7 @@ from ._lib import (  # noqa: F401
     accept_workspace_bytes,
     alloc_workspace,
     attn_dims,
+    dvl_allocate_pack,
     load,
     status_string,
     validate_metadata,

@@ -19,7 +19,8 @@ DSV_F32 = 0
 DSV_BF16 = 1
 MAX_QLEN = 16
 PAGE_SIZE = 16
-TIMING_KINDS = ("attn_split", "attn_combine", "accept_argmax", "accept_prefix")
+TIMING_KINDS = ("attn_split", "attn_combine", "accept_argmax", "accept_prefix", "dvl")
+DVL_MAX_REQS = 1024
 
 
 class DSVError(RuntimeError):
@@ -60,6 +61,7 @@ def load():
         "dsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
         "dsv_accept": (ctypes.c_int, [P, I32, P, P, P, P, I32, I32, I32, P, SZ, P]),
         "dsv_validate_metadata": (ctypes.c_int, [P, P, P, PD, P, P]),
+        "dsv_dvl_allocate_pack": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P, P, I32, I32, P]),
         "dsv_graph_capture_begin": (ctypes.c_int, [P]),
         "dsv_graph_capture_end": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_void_p)]),
         "dsv_graph_replay": (ctypes.c_int, [P, P]),
@@ -204,6 +206,43 @@ def validate_metadata(cu_qlens, ctx_lens, page_table, dims: AttnDims, err_word,
     _check("dsv_validate_metadata", load().dsv_validate_metadata(
         _ptr(cu_qlens), _ptr(ctx_lens), _ptr(page_table), ctypes.byref(dims),
         _ptr(err_word), _stream_handle(stream)))
+
+
+def dvl_allocate_pack(pred_logits, num_live, tokens, positions, kv_refs, k_out, cu_qlens,
+                      packed_tokens, packed_positions, packed_kv_refs, scores_out=None, *,
+                      stream=None) -> None:
+    """Enqueue ``dsv_dvl_allocate_pack`` (Sec. III-C, Alg. 1).
+
+    ``pred_logits`` float32 [N_bs, W-1]; ``num_live`` int32 [1] (device);
+    ``tokens``, ``positions``, ``kv_refs`` int32 [N_bs, W]; ``k_out`` int32
+    [N_bs]; ``cu_qlens`` int32 [N_bs+1]; packed outputs int32 [W*N_bs/2];
+    ``scores_out`` float32 [N_bs, W] or None."""
+    import torch
+    _require(pred_logits, "pred_logits", (torch.float32,), 2)
+    n_bs, wm1 = pred_logits.shape
+    w = wm1 + 1
+    _require(num_live, "num_live", (torch.int32,), 1)
+    for t, n in ((tokens, "tokens"), (positions, "positions"), (kv_refs, "kv_refs")):
+        _require(t, n, (torch.int32,), 2)
+        if tuple(t.shape) != (n_bs, w):
+            raise ValueError("%s must be [N_bs, W]" % n)
+    for t, n, size in ((k_out, "k_out", n_bs), (cu_qlens, "cu_qlens", n_bs + 1),
+                       (packed_tokens, "packed_tokens", w * n_bs // 2),
+                       (packed_positions, "packed_positions", w * n_bs // 2),
+                       (packed_kv_refs, "packed_kv_refs", w * n_bs // 2)):
+        _require(t, n, (torch.int32,), 1)
+        if t.numel() != size:
+            raise ValueError("%s must have %d entries" % (n, size))
+    if num_live.numel() != 1:
+        raise ValueError("num_live must hold one int32")
+    if scores_out is not None:
+        _require(scores_out, "scores_out", (torch.float32,), 2)
+        if tuple(scores_out.shape) != (n_bs, w):
+            raise ValueError("scores_out must be [N_bs, W]")
+    _check("dsv_dvl_allocate_pack", load().dsv_dvl_allocate_pack(
+        _ptr(pred_logits), _ptr(num_live), _ptr(tokens), _ptr(positions), _ptr(kv_refs),
+        _ptr(k_out), _ptr(cu_qlens), _ptr(packed_tokens), _ptr(packed_positions),
+        _ptr(packed_kv_refs), _ptr(scores_out), n_bs, w, _stream_handle(stream)))
 
 
 class Graph:

@@ -146,6 +146,26 @@ int dsv_validate_metadata(const int32_t *cu_qlens, const int32_t *ctx_lens,
   return hipGetLastError() == hipSuccess ? DSV_OK : DSV_ERR_HIP;
 }
 
+int dsv_dvl_allocate_pack(const float *pred_logits, const int32_t *num_live,
+                          const int32_t *tokens, const int32_t *positions,
+                          const int32_t *kv_refs, int32_t *k_out,
+                          int32_t *cu_qlens, int32_t *packed_tokens,
+                          int32_t *packed_positions, int32_t *packed_kv_refs,
+                          float *scores_out, int32_t bucket_reqs,
+                          int32_t block_width, void *hip_stream) {
+  if (!pred_logits || !num_live || !tokens || !positions || !kv_refs || !k_out ||
+      !cu_qlens || !packed_tokens || !packed_positions || !packed_kv_refs)
+    return DSV_ERR_NULL;
+  if (bucket_reqs < 1 || bucket_reqs > DSV_DVL_MAX_REQS) return DSV_ERR_DIMS;
+  if (block_width < 2 || block_width > DSV_MAX_QLEN || block_width % 2 != 0)
+    return DSV_ERR_DIMS;
+  const hipError_t e = launch_dvl(pred_logits, num_live, tokens, positions, kv_refs,
+                                  k_out, cu_qlens, packed_tokens, packed_positions,
+                                  packed_kv_refs, scores_out, bucket_reqs, block_width,
+                                  (hipStream_t)hip_stream);
+  return e == hipSuccess ? DSV_OK : DSV_ERR_HIP;
+}
+
 int dsv_graph_capture_begin(void *hip_stream) {
   if (!hip_stream) return DSV_ERR_NULL;
   const hipError_t e =

@@ -67,8 +67,23 @@ hipError_t launch_validate(const int32_t *cu, const int32_t *ctx,
                            const int32_t *page_table, const dsv_attn_dims &d,
                            int32_t *err_word, hipStream_t s);
 
+// -------------------------------------------------------------------------
+// DVL allocation and packing
+// -------------------------------------------------------------------------
+hipError_t launch_dvl(const float *pred_logits, const int32_t *num_live,
+                      const int32_t *tokens, const int32_t *positions,
+                      const int32_t *kv_refs, int32_t *k_out, int32_t *cu,
+                      int32_t *ptok, int32_t *ppos, int32_t *pref, float *scores,
+                      int32_t n_bs, int32_t w, hipStream_t s);
+
 // Kernel kinds of the timing hook (see dsv_timing_start).
-enum TimingKind { kTimeAttnSplit = 0, kTimeAttnCombine = 1, kTimeArgmax = 2, kTimePrefix = 3 };
+enum TimingKind {
+  kTimeAttnSplit = 0,
+  kTimeAttnCombine = 1,
+  kTimeArgmax = 2,
+  kTimePrefix = 3,
+  kTimeDvl = 4
+};
 // Records a HIP event before (end = false) or after (end = true) a launch
 // when timing is on and the stream is not being captured.
 void timing_mark(int kind, bool end, hipStream_t s);

@@ -99,3 +99,36 @@ class AcceptDev:
     def result(self):
         torch.cuda.synchronize()
         return self.a.cpu().numpy(), self.nxt.cpu().numpy()
+
+
+class DvlDev:
+    """A DvlInputs uploaded once; `run()` enqueues dvl_allocate_pack into
+    buffers pre-filled with a poison value (so unwritten entries show)."""
+
+    POISON = -123456
+
+    def __init__(self, d: W.DvlInputs):
+        self.d = d
+        n_bs, w = d.tokens.shape
+        m_bs = w * n_bs // 2
+        self.logits = torch.from_numpy(np.ascontiguousarray(d.pred_logits)).to(DEV)
+        self.num_live = i32_dev([d.n_live])
+        self.tokens = i32_dev(d.tokens)
+        self.positions = i32_dev(d.positions)
+        self.kv_refs = i32_dev(d.kv_refs)
+        full = lambda n: torch.full((n,), self.POISON, dtype=torch.int32, device=DEV)
+        self.k = full(n_bs)
+        self.cu = full(n_bs + 1)
+        self.ptok, self.ppos, self.pref = full(m_bs), full(m_bs), full(m_bs)
+        self.scores = torch.full((n_bs, w), float("nan"), dtype=torch.float32, device=DEV)
+
+    def run(self, stream=None, scores=True):
+        dsv.dvl_allocate_pack(self.logits, self.num_live, self.tokens, self.positions,
+                              self.kv_refs, self.k, self.cu, self.ptok, self.ppos, self.pref,
+                              self.scores if scores else None, stream=stream)
+
+    def result(self):
+        torch.cuda.synchronize()
+        return dict(k=self.k.cpu().numpy(), offsets=self.cu.cpu().numpy(),
+                    tokens=self.ptok.cpu().numpy(), positions=self.ppos.cpu().numpy(),
+                    kv_refs=self.pref.cpu().numpy(), q=self.scores.cpu().numpy())

@@ -144,3 +144,19 @@ def test_binding_refuses_host_tensors():
                         torch.zeros(1, 2, 1, 1024, dtype=torch.bfloat16),
                         torch.zeros(1, 1, dtype=torch.int32),
                         torch.zeros(1, dtype=torch.int32), q.clone())
+
+
+def test_dvl_rejects_bad_arguments():
+    lib = dsv.load()
+    fake = 1 << 20
+    args = [fake] * 10 + [None, 32, 16, None]
+    bad = list(args); bad[0] = None
+    assert lib.dsv_dvl_allocate_pack(*bad) == -1
+    bad = list(args); bad[9] = None
+    assert lib.dsv_dvl_allocate_pack(*bad) == -1
+    for n_bs in (0, dsv.DVL_MAX_REQS + 1):
+        bad = list(args); bad[11] = n_bs
+        assert lib.dsv_dvl_allocate_pack(*bad) == -2
+    for w in (0, 1, 3, 15, 18):
+        bad = list(args); bad[12] = w
+        assert lib.dsv_dvl_allocate_pack(*bad) == -2
