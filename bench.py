@@ -184,6 +184,54 @@ def stress_bench(steps):
             "acceptance_exact_every_step": exact}
 
 
+def dvl_bench(launches=100, replays=10):
+    """DVL allocate-and-pack (Sec. III-C, Alg. 1) per launch: ``launches``
+    back-to-back calls captured in one hipGraph, replayed ``replays`` times
+    and timed with HIP events on the capturing stream, for the B=32 bucket of
+    the workload and two larger buckets.  Inputs: make_dvl_inputs (synthetic
+    predictor logits with per-request geometric profiles), all slots live.
+    The kernel is one workgroup, so it is bound by latency, not by HBM: the
+    bytes are given for reference only."""
+    import torch
+
+    import paper_2609_37532_amd as dsv
+    import workloads as W
+
+    out = {}
+    for n_bs in (32, 256, 1024):
+        w = W.BLOCK_WIDTH
+        d = W.make_dvl_inputs(np.random.default_rng(W.SEED_BASE + 60 + n_bs), n_bs=n_bs,
+                              n_live=n_bs)
+        m_bs = w * n_bs // 2
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+        lg, tok, pos, ref = dev(d.pred_logits), dev(d.tokens), dev(d.positions), dev(d.kv_refs)
+        nl = dev(np.array([n_bs], np.int32))
+        z = lambda n: torch.zeros(n, dtype=torch.int32, device="cuda")
+        k, cu, pt, pp, pr = z(n_bs), z(n_bs + 1), z(m_bs), z(m_bs), z(m_bs)
+        s = torch.cuda.Stream()
+        call = lambda: dsv.dvl_allocate_pack(lg, nl, tok, pos, ref, k, cu, pt, pp, pr, stream=s)
+        for _ in range(10):
+            call()
+        torch.cuda.synchronize()
+        g = dsv.Graph().capture(lambda: [call() for _ in range(launches)], s)
+        g.replay(s)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(replays):
+            g.replay(s)
+        e1.record(s)
+        torch.cuda.synchronize()
+        g.close()
+        us = e0.elapsed_time(e1) * 1e3 / (launches * replays)
+        nbytes = n_bs * (w - 1) * 4 + 3 * m_bs * 4 + 8 + (2 * n_bs + 1) * 4 + 3 * m_bs * 4
+        out["n_bs_%d" % n_bs] = {"us_per_call": round(us, 2), "algorithmic_bytes": nbytes}
+    out["bound"] = "latency (one workgroup)"
+    out["timing"] = "%d launches in one hipGraph, %d replays, HIP events" % (launches, replays)
+    return out
+
+
 def copy_probe():
     """Three device-to-device copies of 1 GiB: reads and writes 2^30 bytes
     each, the known size against which FETCH_SIZE / WRITE_SIZE are scaled."""
@@ -348,6 +396,8 @@ def main():
 
     del q, kv, logits, out
     torch.cuda.empty_cache()
+    log("DVL allocate-and-pack ...")
+    result["dvl"] = dvl_bench()
     if not args.no_stress:
         log("stress run (36 layers, %d steps) ..." % args.stress_steps)
         result["stress"] = stress_bench(args.stress_steps)

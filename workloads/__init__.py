@@ -8,6 +8,7 @@ argmax).  Expected acceptance results it returns are known by construction
 """
 from .gen import (  # noqa: F401
     BF16_NAN,
+    BLOCK_WIDTH,
     SEED_BASE,
     AcceptInputs,
     AttnInputs,
