@@ -232,6 +232,84 @@ def dvl_bench(launches=100, replays=10):
     return out
 
 
+def bucket_bench(layers=4, reps=5):
+    """The multi-bucket capture set (Sec. III-D, Alg. 2, Eqs. (13)-(15)):
+    buckets {8, 16, 32, 64} sharing one attention and one acceptance
+    workspace, each with a captured decision graph (DVL) and verify graph
+    (``layers`` attention layers, Qwen3-8B shape, then acceptance over
+    151,936 tokens).  Per bucket, at N = N_bs and at N = 3 N_bs / 4 (the rest
+    sentinels): decision and verify replay times (HIP events on the replay
+    stream, mean of ``reps`` steps; staging outside the timed region), plus
+    the set's device memory.  Contexts U[1024, 8192] as in the workload."""
+    import torch
+
+    import paper_2609_37532_amd as dsv
+    import workloads as W
+
+    sizes = (8, 16, 32, 64)
+    rng = np.random.default_rng(W.SEED_BASE + 80)
+    hq, hkv, d, V = 32, 8, 128, 151936
+    ctx_lo, ctx_hi = 1024, 8192
+    pool = max(sizes)
+    max_kv_len = ctx_hi + W.BLOCK_WIDTH
+    max_pages = -(-max_kv_len // W.PAGE_SIZE)
+    num_pages = pool * max_pages
+    cache_map = rng.permutation(num_pages).astype(np.int32).reshape(pool, max_pages)
+    ctx_all = rng.integers(ctx_lo, ctx_hi + 1, size=pool).astype(np.int32)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(W.SEED_BASE + 81)
+    kv = [torch.randn((num_pages, 2, hkv, W.PAGE_SIZE * d), generator=gen, device="cuda",
+                      dtype=torch.bfloat16) for _ in range(layers)]
+    bs = dsv.BucketSet(sizes, kv_pools=kv, max_pages=max_pages, max_kv_len=max_kv_len,
+                       num_q_heads=hq, head_dim=d, vocab=V)
+    s = torch.cuda.Stream()
+    bs.capture(s)
+    rows = []
+    for b in sizes:
+        bk = bs[b]
+        bk.q.normal_(generator=gen)
+        bk.logits.normal_(generator=gen)
+        for n in (b, 3 * b // 4):
+            t_dec, t_ver, kv_tokens = [], [], 0
+            for _ in range(reps):
+                reqs = np.sort(rng.choice(pool, size=n, replace=False))
+                dv = W.make_dvl_inputs(rng, n_bs=b, n_live=n)
+                bk.stage_decision(n, dv.pred_logits, dv.tokens, dv.positions, dv.kv_refs)
+                bk.stage_verify(n, ctx_all[reqs], cache_map[reqs])
+                torch.cuda.synchronize()
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                ev[0].record(s)
+                bk.graph_dec.replay(s)
+                ev[1].record(s)
+                bk.graph_ver.replay(s)
+                ev[2].record(s)
+                torch.cuda.synchronize()
+                t_dec.append(ev[0].elapsed_time(ev[1]))
+                t_ver.append(ev[1].elapsed_time(ev[2]))
+                kv_tokens += int(ctx_all[reqs].sum()) + 8 * n
+            ver_ms = float(np.mean(t_ver))
+            rows.append({"n_bs": b, "live": n, "capacity_rows": 8 * b,
+                         "decision_replay_us": round(float(np.mean(t_dec)) * 1e3, 2),
+                         "verify_replay_us": round(ver_ms * 1e3, 2),
+                         "verify_us_per_layer_incl_accept": round(ver_ms * 1e3 / layers, 2),
+                         "packed_tokens_per_s": round(8 * n / (ver_ms * 1e-3), 1),
+                         "kv_gbps": round(kv_tokens / reps * hkv * d * 4 * layers
+                                          / (ver_ms * 1e-3) / 1e9, 1)})
+    mem = bs.memory()
+    bs.close()
+    del kv
+    torch.cuda.empty_cache()
+    return {"workload": "%d layers of Qwen3-8B-shape verify attention + acceptance over "
+                        "151936 tokens per bucket; DVL lengths fill 8 rows per live request"
+                        % layers,
+            "steps": rows, "memory": mem["total"],
+            "memory_per_bucket": [{k: m[k] for k in ("n_bs", "metadata_bytes",
+                                                     "activation_bytes",
+                                                     "graph_decision_bytes",
+                                                     "graph_verify_bytes")}
+                                  for m in mem["buckets"]]}
+
+
 def copy_probe():
     """Three device-to-device copies of 1 GiB: reads and writes 2^30 bytes
     each, the known size against which FETCH_SIZE / WRITE_SIZE are scaled."""
@@ -398,6 +476,8 @@ def main():
     torch.cuda.empty_cache()
     log("DVL allocate-and-pack ...")
     result["dvl"] = dvl_bench()
+    log("bucket set ...")
+    result["buckets"] = bucket_bench()
     if not args.no_stress:
         log("stress run (36 layers, %d steps) ..." % args.stress_steps)
         result["stress"] = stress_bench(args.stress_steps)

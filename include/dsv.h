@@ -242,9 +242,9 @@ int dsv_validate_metadata(const int32_t *cu_qlens, const int32_t *ctx_lens,
  * is deterministic and independent of the launch.
  *
  * Arguments (device pointers unless stated):
- *   pred_logits      fp32 [N_bs][W-1], predictor outputs (Eq. (5)); rows of
- *                    sentinel slots are not read.  A NaN logit leaves the
- *                    running minimum unchanged.
+ *   pred_logits      fp32 [N_bs][W-1], predictor outputs (Eq. (5)); the
+ *                    values in rows of sentinel slots are not used.  A NaN
+ *                    logit leaves the running minimum unchanged.
  *   num_live         int32 scalar N, read on the device (so a captured graph
  *                    can replay with another live count); values outside
  *                    [0, N_bs] are clamped into it (N = 0 gives M_live = 0).

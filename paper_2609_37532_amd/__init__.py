@@ -13,6 +13,9 @@ and the decision step that produces their packed layout:
 * ``dvl_allocate_pack(...)`` -- DVL budget allocation and flat-buffer packing
   (verify lengths under the shared budget, the offsets, the packed rows).
 
+``BucketSet`` holds fixed-address buffers and the captured decision and
+verify graphs for a set of request-bucket sizes (``select_bucket``).
+
 This module only marshals arguments; PyTorch provides device memory and
 streams.  ``Graph`` captures and replays the calls with fixed buffer
 addresses; ``KernelTimer`` times the kernels with HIP events.
@@ -40,3 +43,4 @@ from ._lib import (  # noqa: F401
     verify_attn,
     verify_attn_workspace_bytes,
 )
+from .buckets import Bucket, BucketSet, select_bucket  # noqa: F401,E402

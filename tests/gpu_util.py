@@ -132,3 +132,16 @@ class DvlDev:
         return dict(k=self.k.cpu().numpy(), offsets=self.cu.cpu().numpy(),
                     tokens=self.ptok.cpu().numpy(), positions=self.ppos.cpu().numpy(),
                     kv_refs=self.pref.cpu().numpy(), q=self.scores.cpu().numpy())
+
+
+def gather_oracle_inputs(q_rows, kv_pool, page_row, ctx, k):
+    """Host inputs of one request for the attention oracle: its q rows
+    [k, Hq, D], its pages gathered from the device pool (renumbered 0..),
+    a one-row page table, its context and offsets."""
+    npg = -(-(int(ctx) + int(k)) // W.PAGE_SIZE)
+    ids = torch.as_tensor(np.asarray(page_row[:npg], dtype=np.int64), device=kv_pool.device)
+    as_bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    return dict(q=as_bits(q_rows), cu_qlens=np.array([0, k], np.int32),
+                kv_pages=as_bits(kv_pool[ids]),
+                page_table=np.arange(npg, dtype=np.int32)[None, :],
+                ctx_lens=np.array([ctx], np.int32))

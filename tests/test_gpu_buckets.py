@@ -1,0 +1,114 @@
+"""GPU: the multi-bucket capture set (Sec. III-D, Alg. 2, Eqs. (13)-(15)).
+
+Buckets {4, 8, 16, 32}; two Qwen3-8B-shaped attention layers (32q/8kv,
+D=128, page 16) and acceptance over a 32,000-token vocabulary.  A pool of 32
+requests shrinks step by step; each step picks the bucket (Eq. (14)),
+replays that bucket's decision graph (DVL allocation and packing) and then
+its verify graph (attention for both layers, then acceptance), which reads
+the offsets and packed tokens the decision graph wrote.  Checked per step:
+the bucket choice; the decision outputs bit-exact against the oracle; the
+acceptance of live requests against planted values and the sentinels' 0 / -1;
+tail rows of the attention output zero; sampled attention rows against the
+fp64 oracle (max-abs 1e-2, mean-abs 1e-3).
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+try:
+    import torch
+
+    import paper_2609_37532_amd as dsv
+    from gpu_util import DEV, gather_oracle_inputs, say
+except Exception:  # pragma: no cover
+    pass
+
+BUCKETS = (4, 8, 16, 32)
+LIVE_COUNTS = (32, 29, 16, 11, 8, 5, 4, 3, 1, 17)
+HQ, HKV, D, V, L = 32, 8, 128, 32000, 2
+CTX = (256, 2048)
+
+
+def test_bucket_set_decision_then_verify():
+    rng = np.random.default_rng(W.SEED_BASE + 70)
+    pool_reqs = 32
+    max_kv_len = CTX[1] + W.BLOCK_WIDTH
+    max_pages = -(-max_kv_len // W.PAGE_SIZE)
+    num_pages = pool_reqs * max_pages
+    cache_map = rng.permutation(num_pages).astype(np.int32).reshape(pool_reqs, max_pages)
+    ctx_all = rng.integers(CTX[0], CTX[1] + 1, size=pool_reqs).astype(np.int32)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(W.SEED_BASE + 71)
+    kv_pools = [torch.randn((num_pages, 2, HKV, W.PAGE_SIZE * D), generator=gen, device=DEV,
+                            dtype=torch.bfloat16) for _ in range(L)]
+    bs = dsv.BucketSet(BUCKETS, kv_pools=kv_pools, max_pages=max_pages, max_kv_len=max_kv_len,
+                       num_q_heads=HQ, head_dim=D, vocab=V)
+    s = torch.cuda.Stream(device=DEV)
+    bs.capture(s)
+    try:
+        mem = bs.memory()
+        for m in mem["buckets"]:
+            say("buckets", "memory", m)
+            assert m["capacity_rows"] == 8 * m["n_bs"]
+        say("buckets", "memory total", mem["total"])
+        assert all(bs[b].ws_attn.data_ptr() == bs.ws_attn.data_ptr() for b in BUCKETS)
+        for step, n in enumerate(LIVE_COUNTS):
+            b = bs.select(n)
+            assert b == min(x for x in BUCKETS if x >= n)
+            say("buckets", "step", step, "live", n, "bucket", b)
+            bk = bs[b]
+            reqs = np.sort(rng.choice(pool_reqs, size=n, replace=False))
+            d = W.make_dvl_inputs(rng, n_bs=b, n_live=n, vocab=V)
+            bk.stage_decision(n, d.pred_logits, d.tokens, d.positions, d.kv_refs)
+            bk.replay_decision(s)
+            s.synchronize()
+            k = bk.k.cpu().numpy()
+            cu = bk.cu.cpu().numpy()
+            packed = bk.packed_tokens.cpu().numpy()
+            ref = oracle.dvl_allocate_pack(d.pred_logits, n, d.tokens, d.positions, d.kv_refs)
+            assert np.array_equal(k, ref["k"]) and np.array_equal(cu, ref["offsets"])
+            assert np.array_equal(packed, ref["tokens"])
+            assert np.array_equal(bk.packed_kv_refs.cpu().numpy(), ref["kv_refs"])
+            assert int(cu[-1]) == 8 * n and (k[n:] == 0).all()
+
+            # verify inputs: request state, target activations, planted logits
+            bk.stage_verify(n, ctx_all[reqs], cache_map[reqs])
+            bk.q.normal_(generator=gen)
+            bk.out.fill_(float("nan"))
+            bk.logits.normal_(generator=gen)
+            a_ref, nxt_ref, rows, toks = W.plant_boosts(rng, cu, packed, V, 0.3)
+            r = torch.as_tensor(rows, device=DEV)
+            t = torch.as_tensor(toks, device=DEV)
+            bk.logits.index_put_((r, t), torch.full(r.shape, 10.0, dtype=bk.logits.dtype,
+                                                    device=DEV), accumulate=True)
+            bk.replay_verify(s)
+            s.synchronize()
+            a = bk.accept_len.cpu().numpy()
+            nxt = bk.next_token.cpu().numpy()
+            assert np.array_equal(a, a_ref) and np.array_equal(nxt, nxt_ref)
+            assert (a[n:] == 0).all() and (nxt[n:] == -1).all()
+            out = bk.out.float()
+            assert torch.all(out[:, 8 * n:] == 0).item(), "tail rows not zero"
+            # sampled rows against the oracle: first and last live slot
+            for layer in range(L):
+                for slot in sorted({0, n - 1}):
+                    o, kk = int(cu[slot]), int(k[slot])
+                    g = gather_oracle_inputs(bk.q[layer, o:o + kk], kv_pools[layer],
+                                             cache_map[reqs[slot]], ctx_all[reqs[slot]], kk)
+                    want = oracle.verify_attn(g["q"], g["cu_qlens"], g["kv_pages"],
+                                              g["page_table"], g["ctx_lens"], num_q_heads=HQ,
+                                              num_kv_heads=HKV, head_dim=D, page_size=16,
+                                              scale=1.0 / math.sqrt(D))
+                    got = out[layer, o:o + kk].cpu().numpy().astype(np.float64)
+                    err = np.abs(got - want)
+                    assert np.isfinite(got).all()
+                    assert err.max() <= 1e-2 and err.mean() <= 1e-3, (step, layer, slot)
+            say("buckets", "step", step, "ok")
+    finally:
+        bs.close()

@@ -9,6 +9,7 @@ argmax).  Expected acceptance results it returns are known by construction
 from .gen import (  # noqa: F401
     BF16_NAN,
     BLOCK_WIDTH,
+    PAGE_SIZE,
     SEED_BASE,
     AcceptInputs,
     AttnInputs,
@@ -29,4 +30,5 @@ from .gen import (  # noqa: F401
     StressStep,
     DvlInputs,
     make_dvl_inputs,
+    plant_boosts,
 )

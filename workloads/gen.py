@@ -416,6 +416,39 @@ CONFIGS[5] = dict(name="graph-replay stress", num_layers=36, num_reqs=32, num_q_
                   steps=100, vocab=151936, accept_dtype="bf16", p_accept=0.3)
 
 
+def plant_boosts(rng: np.random.Generator, cu_qlens, draft_tokens, vocab: int,
+                 p_accept: float):
+    """The planted acceptance of :func:`make_accept_inputs` for drafts that
+    are already given, as a list of logit boosts to add on the device: per
+    live request (o = cu[i], k = k_i) a_i = min(G - 1, k - 1) with
+    G ~ Geometric(p_accept); rows o+j (j < a_i) boost draft[o+j+1]; row o+a_i
+    boosts a token x_i != draft[o+a_i+1] (any token when a_i = k-1).
+    Returns (accept_len, next_token, boost_rows, boost_tokens)."""
+    cu = np.asarray(cu_qlens, dtype=np.int64)
+    draft = np.asarray(draft_tokens)
+    B = cu.shape[0] - 1
+    a = np.zeros(B, dtype=np.int32)
+    nxt = np.full(B, -1, dtype=np.int32)
+    rows, toks = [], []
+    for i in range(B):
+        o, kk = int(cu[i]), int(cu[i + 1] - cu[i])
+        if kk == 0:
+            continue
+        a[i] = min(int(rng.geometric(p_accept)) - 1, kk - 1)
+        for j in range(int(a[i])):
+            rows.append(o + j)
+            toks.append(int(draft[o + j + 1]))
+        if a[i] < kk - 1:
+            avoid = int(draft[o + a[i] + 1])
+            x = (avoid + 1 + int(rng.integers(0, vocab - 1))) % vocab
+        else:
+            x = int(rng.integers(0, vocab))
+        nxt[i] = x
+        rows.append(o + int(a[i]))
+        toks.append(x)
+    return a, nxt, np.asarray(rows, np.int64), np.asarray(toks, np.int64)
+
+
 @dataclass
 class StressStep:
     """One step's inputs: verify lengths, packed offsets, packed draft tokens,
@@ -461,28 +494,9 @@ class StressPlan:
         k = verify_lengths(self.rng, B, cap, p=0.25)
         cu = cu_from_lengths(k)
         draft = self.rng.integers(0, V, size=cap, dtype=np.int64).astype(np.int32)
-        a = np.zeros(B, dtype=np.int32)
-        nxt = np.full(B, -1, dtype=np.int32)
-        rows, toks = [], []
-        for i in range(B):
-            o, kk = int(cu[i]), int(k[i])
-            if kk == 0:
-                continue
-            a[i] = min(int(self.rng.geometric(self.p_accept)) - 1, kk - 1)
-            for j in range(int(a[i])):
-                rows.append(o + j)
-                toks.append(int(draft[o + j + 1]))
-            if a[i] < kk - 1:
-                avoid = int(draft[o + a[i] + 1])
-                x = (avoid + 1 + int(self.rng.integers(0, V - 1))) % V
-            else:
-                x = int(self.rng.integers(0, V))
-            nxt[i] = x
-            rows.append(o + int(a[i]))
-            toks.append(x)
+        a, nxt, rows, toks = plant_boosts(self.rng, cu, draft, V, self.p_accept)
         return StressStep(qlens=k, cu_qlens=cu, draft_tokens=draft, planted_accept_len=a,
-                          planted_next=nxt, boost_rows=np.asarray(rows, np.int64),
-                          boost_tokens=np.asarray(toks, np.int64))
+                          planted_next=nxt, boost_rows=rows, boost_tokens=toks)
 
 
 # --------------------------------------------------------------------- DVL
