@@ -53,6 +53,14 @@ def _load():
     lib.oracle_row_argmax.restype = ctypes.c_int
     lib.oracle_accept.argtypes = [p, i32, p, p, p, p, i32, i32, i32]
     lib.oracle_accept.restype = ctypes.c_int
+    lib.oracle_accept_stochastic.argtypes = [p, i32, p, p, p, ctypes.c_double, p, p, p,
+                                             i32, i32, i32]
+    lib.oracle_accept_stochastic.restype = ctypes.c_int
+    lib.oracle_dvl_scores.argtypes = [p, i32, i32, p, p, p]
+    lib.oracle_dvl_adjust.argtypes = [p, p, i32, i32, i32, p, p]
+    lib.oracle_dvl_pack.argtypes = [p, i32, i32, i32, i32, p, p, p, p, p, p, p, p]
+    for f in (lib.oracle_dvl_scores, lib.oracle_dvl_adjust, lib.oracle_dvl_pack):
+        f.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -201,3 +209,25 @@ def dvl_allocate_pack(pred_logits, n_live, tokens, positions, kv_refs, w=16):
     res = dvl_pack(k, n_bs, w, w * n_bs // 2, tokens, positions, kv_refs)
     res.update(q=q, k0=k0, ell=ell, updates=upd)
     return res
+
+
+def accept_stochastic(logits, dtype, cu_qlens, draft_tokens, uniforms, temperature):
+    """Stochastic prefix verifier (Sec. III-D); ``uniforms`` float32 [cap, 2].
+    Returns ``(accept_len, next_token, margin)``."""
+    lib = _load()
+    lg, code = _logits_args(logits, dtype)
+    cu = _c(cu_qlens, np.int32)
+    dr = _c(draft_tokens, np.int32)
+    un = _c(uniforms, np.float32)
+    cap, vocab = lg.shape
+    assert un.shape == (cap, 2)
+    B = cu.shape[0] - 1
+    a = np.empty(B, dtype=np.int32)
+    nxt = np.empty(B, dtype=np.int32)
+    mg = np.empty(B, dtype=np.float64)
+    rc = lib.oracle_accept_stochastic(_ptr(lg), code, _ptr(cu), _ptr(dr), _ptr(un),
+                                      ctypes.c_double(float(temperature)), _ptr(a), _ptr(nxt),
+                                      _ptr(mg), B, cap, vocab)
+    if rc != 0:
+        raise ValueError("oracle_accept_stochastic rejected its input (rc=%d)" % rc)
+    return a, nxt, mg

@@ -324,3 +324,110 @@ int oracle_dvl_pack(const int32_t *k_live, int32_t n, int32_t n_bs, int32_t w,
   }
   return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Stochastic prefix verifier (Sec. III-D "Prefix verifier", temperature T>0).
+ *
+ * The target policy at a row is P = softmax(logits / T).  Request i's
+ * candidates are tested in order: candidate x_j = draft[o+j+1] is accepted
+ * with probability P_{o+j}(x_j), decided by the caller's uniform u[o+j][0]
+ * (accepted iff u < P(x)).  At the first rejection (row o+a) the successor
+ * is drawn from P_{o+a} with x_a removed and the rest renormalised; if all
+ * k-1 candidates pass, from P_{o+k-1} unchanged.  The draw inverts the
+ * cumulative distribution in index order with u[o+a][1]: the successor is
+ * the smallest v whose cumulative probability exceeds u.  A candidate id
+ * outside [0, vocab) has probability 0 and removes nothing.
+ *
+ * margin[i] (if not NULL) receives the smallest distance, in probability,
+ * between one of the request's uniforms and the threshold its decision
+ * compared it with (+inf for a sentinel): how far the result is from
+ * flipping under a perturbation of the probabilities.
+ * ---------------------------------------------------------------------- */
+
+/* P(v) for one row: writes prob[0..vocab) (double), returns 0. */
+static void row_softmax(const void *logits, int32_t dtype, int64_t base, int32_t vocab,
+                        double inv_t, double *prob) {
+  double m = -INFINITY;
+  for (int32_t v = 0; v < vocab; ++v) {
+    double x = logit_at(logits, dtype, base + v) * inv_t;
+    if (x > m) m = x;
+  }
+  double z = 0.0;
+  for (int32_t v = 0; v < vocab; ++v) {
+    prob[v] = exp(logit_at(logits, dtype, base + v) * inv_t - m);
+    z += prob[v];
+  }
+  for (int32_t v = 0; v < vocab; ++v) prob[v] /= z;
+}
+
+int oracle_accept_stochastic(const void *logits, int32_t dtype,
+                             const int32_t *cu_qlens, const int32_t *draft_tokens,
+                             const float *uniforms, double temperature,
+                             int32_t *accept_len, int32_t *next_token,
+                             double *margin, int32_t num_reqs, int32_t cap,
+                             int32_t vocab) {
+  if (!logits || !cu_qlens || !draft_tokens || !uniforms || !accept_len || !next_token)
+    return -1;
+  if (num_reqs < 1 || cap < 1 || vocab < 1 || (dtype != 0 && dtype != 1)) return -1;
+  if (!(temperature > 0.0) || !isfinite(temperature)) return -1;
+  if (cu_qlens[0] != 0 || cu_qlens[num_reqs] > cap) return -1;
+  for (int32_t i = 0; i < num_reqs; ++i)
+    if (cu_qlens[i + 1] < cu_qlens[i] || cu_qlens[i + 1] - cu_qlens[i] > 64) return -1;
+  double inv_t = 1.0 / temperature;
+  double *prob = (double *)malloc(sizeof(double) * (size_t)vocab);
+  if (!prob) return -1;
+  for (int32_t i = 0; i < num_reqs; ++i) {
+    int32_t o = cu_qlens[i];
+    int32_t k = cu_qlens[i + 1] - o;
+    double mg = INFINITY;
+    if (k == 0) {
+      accept_len[i] = 0;
+      next_token[i] = -1;
+      if (margin) margin[i] = mg;
+      continue;
+    }
+    /* accept candidates while the uniform falls below their probability */
+    int32_t a = 0;
+    int32_t removed = -1;
+    while (a < k - 1) {
+      row_softmax(logits, dtype, (int64_t)(o + a) * vocab, vocab, inv_t, prob);
+      int32_t x = draft_tokens[o + a + 1];
+      double px = (x >= 0 && x < vocab) ? prob[x] : 0.0;
+      double u = (double)uniforms[2 * (int64_t)(o + a)];
+      if (fabs(u - px) < mg) mg = fabs(u - px);
+      if (u < px) {
+        ++a;
+      } else {
+        removed = (x >= 0 && x < vocab) ? x : -1;
+        break;
+      }
+    }
+    /* successor: P at row o+a, without the rejected candidate if any */
+    row_softmax(logits, dtype, (int64_t)(o + a) * vocab, vocab, inv_t, prob);
+    double total = 1.0;
+    if (removed >= 0) {
+      total -= prob[removed];
+      prob[removed] = 0.0;
+    }
+    double us = (double)uniforms[2 * (int64_t)(o + a) + 1];
+    double cum = 0.0;
+    int32_t pick = -1, last = -1;
+    for (int32_t v = 0; v < vocab; ++v) {
+      if (prob[v] <= 0.0) continue;
+      double before = cum;
+      cum += prob[v] / total;
+      last = v;
+      if (pick < 0 && cum > us) {
+        pick = v;
+        double d = us - before < cum - us ? us - before : cum - us;
+        if (d < mg) mg = d;
+      }
+    }
+    if (pick < 0) pick = last; /* u at or past the rounded total */
+    accept_len[i] = a;
+    next_token[i] = pick;
+    if (margin) margin[i] = mg;
+  }
+  free(prob);
+  return 0;
+}

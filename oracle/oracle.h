@@ -33,6 +33,20 @@ int oracle_accept(const void *logits, int32_t dtype, const int32_t *cu_qlens,
                   int32_t *next_token, int32_t num_reqs, int32_t cap,
                   int32_t vocab);
 
+/* Stochastic prefix verifier (Sec. III-D "Prefix verifier", temperature
+ * T > 0): P = softmax(logits / T) per row; candidate x_j = draft[o+j+1] is
+ * accepted iff uniforms[o+j][0] < P_{o+j}(x_j); the successor is drawn by
+ * inverting the cumulative distribution (index order) of P_{o+a}, without
+ * the rejected candidate if there is one, at uniforms[o+a][1].  uniforms is
+ * float [cap][2].  margin (nullable) receives per request the smallest
+ * distance between a uniform and the threshold it was compared with. */
+int oracle_accept_stochastic(const void *logits, int32_t dtype,
+                             const int32_t *cu_qlens, const int32_t *draft_tokens,
+                             const float *uniforms, double temperature,
+                             int32_t *accept_len, int32_t *next_token,
+                             double *margin, int32_t num_reqs, int32_t cap,
+                             int32_t vocab);
+
 /* ---- DVL budget allocation and flat-buffer packing (Sec. III-C) ----
  *
  * Decisions are taken in single precision, as the library takes them: each
