@@ -13,6 +13,9 @@
  *                    the longest-prefix compare against the drafted tokens
  *                    (Sec. III-D "Prefix verifier", greedy case; Sec. I
  *                    definition of accepted tokens);
+ *   dsv_accept_stochastic
+ *                    the same verifier at temperature > 0: probability-ratio
+ *                    acceptance with residual resampling (Sec. III-D);
  *   dsv_dvl_allocate_pack
  *                    DVL budget allocation and flat-buffer packing (Sec.
  *                    III-C, Alg. 1, Eqs. (6)-(11)): per-request verify
@@ -201,6 +204,44 @@ int dsv_accept(const void *logits_packed, int32_t dtype,
                size_t workspace_bytes, void *hip_stream);
 
 /*
+ * Stochastic acceptance: the prefix verifier at temperature T > 0 (Sec. III-D
+ * "Prefix verifier").  The target policy at packed row r is
+ * P_r = softmax(logits[r] / T).  For request i (o = cu_qlens[i], k = k_i >= 1)
+ * the candidates x_j = draft_tokens[o+j+1], j = 0 .. k-2, are tested in
+ * order: x_j is accepted iff uniforms[o+j][0] < P_{o+j}(x_j); the first
+ * rejection stops the prefix.  accept_len[i] = a is the number accepted.  The
+ * successor is drawn from row o+a: from P_{o+a} with x_a removed and the rest
+ * renormalised if x_a was rejected, from P_{o+k-1} unchanged if every
+ * candidate passed; the draw takes the smallest token whose cumulative
+ * probability (vocabulary order) exceeds uniforms[o+a][1].  For k = 0:
+ * accept_len 0, next_token -1.  Over uniform random uniforms the first
+ * emitted token is distributed as P at the anchor row (the verifier is
+ * lossless).
+ *
+ *   logits_packed  [capacity][vocab] fp32 or bf16 (dtype); each live row
+ *                  has at least one finite logit; -inf logits are allowed
+ *                  (probability 0); NaN and +inf are not.
+ *   uniforms       fp32 [capacity][2], values in [0, 1), device; the caller
+ *                  draws them (e.g. a counter-based generator on the device).
+ *   temperature    host float, > 0 and finite (1/T must be finite).
+ *   draft_tokens   candidate ids outside [0, vocab) have probability 0.
+ *   workspace      >= dsv_accept_stochastic_workspace_bytes(...) bytes,
+ *                  256-byte aligned.
+ * Arithmetic is fp32 and deterministic.  Every decision compares a uniform
+ * with a threshold; it matches exact arithmetic unless the uniform lies
+ * within fp32 rounding of that threshold.  Other arguments and metadata
+ * rules as for dsv_accept.
+ */
+size_t dsv_accept_stochastic_workspace_bytes(int32_t capacity, int32_t num_reqs,
+                                             int32_t vocab);
+int dsv_accept_stochastic(const void *logits_packed, int32_t dtype,
+                          const int32_t *cu_qlens, const int32_t *draft_tokens,
+                          const float *uniforms, float temperature,
+                          int32_t *accept_len, int32_t *next_token, int32_t num_reqs,
+                          int32_t capacity, int32_t vocab, void *workspace,
+                          size_t workspace_bytes, void *hip_stream);
+
+/*
  * Debug check of device metadata (the preconditions listed above).  Enqueues
  * one small kernel that writes, into *err_word (device int32), a bit mask of
  * the violated rules (0 = all hold):
@@ -296,15 +337,17 @@ int dsv_graph_destroy(void *graph_exec);
 /*
  * Kernel timing for measurement harnesses.  After dsv_timing_start(n), the
  * next n kernel launches made by eager (not captured) dsv_verify_attn,
- * dsv_accept and dsv_dvl_allocate_pack calls are bracketed by HIP events
+ * dsv_accept, dsv_accept_stochastic and dsv_dvl_allocate_pack calls are
+ * bracketed by HIP events
  * recorded on the caller's stream.  dsv_timing_stop waits for those events,
  * writes per kernel kind the summed milliseconds and the launch count (arrays
  * of DSV_TIMING_KINDS), and turns timing off.  Kinds: 0 attention split
  * kernel, 1 attention combine kernel, 2 vocabulary argmax kernel,
- * 3 prefix-compare kernel, 4 DVL allocate-and-pack kernel.  Not thread-safe
- * against concurrent calls from several host threads.
+ * 3 prefix-compare kernel, 4 DVL allocate-and-pack kernel, 5 softmax
+ * statistics kernel and 6 stochastic draw kernel of dsv_accept_stochastic.
+ * Not thread-safe against concurrent calls from several host threads.
  */
-#define DSV_TIMING_KINDS 5
+#define DSV_TIMING_KINDS 7
 int dsv_timing_start(int32_t max_launches);
 int dsv_timing_stop(float *total_ms, int32_t *launches);
 

@@ -53,9 +53,12 @@ def _load():
     lib.oracle_row_argmax.restype = ctypes.c_int
     lib.oracle_accept.argtypes = [p, i32, p, p, p, p, i32, i32, i32]
     lib.oracle_accept.restype = ctypes.c_int
-    lib.oracle_accept_stochastic.argtypes = [p, i32, p, p, p, ctypes.c_double, p, p, p,
+    lib.oracle_accept_stochastic.argtypes = [p, i32, p, p, p, ctypes.c_double, p, p, p, p,
                                              i32, i32, i32]
     lib.oracle_accept_stochastic.restype = ctypes.c_int
+    lib.oracle_successor_interval.argtypes = [p, i32, i32, i32, i32, ctypes.c_double, i32,
+                                              p, p]
+    lib.oracle_successor_interval.restype = ctypes.c_int
     lib.oracle_dvl_scores.argtypes = [p, i32, i32, p, p, p]
     lib.oracle_dvl_adjust.argtypes = [p, p, i32, i32, i32, p, p]
     lib.oracle_dvl_pack.argtypes = [p, i32, i32, i32, i32, p, p, p, p, p, p, p, p]
@@ -213,7 +216,7 @@ def dvl_allocate_pack(pred_logits, n_live, tokens, positions, kv_refs, w=16):
 
 def accept_stochastic(logits, dtype, cu_qlens, draft_tokens, uniforms, temperature):
     """Stochastic prefix verifier (Sec. III-D); ``uniforms`` float32 [cap, 2].
-    Returns ``(accept_len, next_token, margin)``."""
+    Returns ``(accept_len, next_token, margin_accept, margin_sample)``."""
     lib = _load()
     lg, code = _logits_args(logits, dtype)
     cu = _c(cu_qlens, np.int32)
@@ -224,10 +227,25 @@ def accept_stochastic(logits, dtype, cu_qlens, draft_tokens, uniforms, temperatu
     B = cu.shape[0] - 1
     a = np.empty(B, dtype=np.int32)
     nxt = np.empty(B, dtype=np.int32)
-    mg = np.empty(B, dtype=np.float64)
+    ma = np.empty(B, dtype=np.float64)
+    ms = np.empty(B, dtype=np.float64)
     rc = lib.oracle_accept_stochastic(_ptr(lg), code, _ptr(cu), _ptr(dr), _ptr(un),
-                                      ctypes.c_double(float(temperature)), _ptr(a), _ptr(nxt),
-                                      _ptr(mg), B, cap, vocab)
+                                      float(temperature), _ptr(a), _ptr(nxt), _ptr(ma),
+                                      _ptr(ms), B, cap, vocab)
     if rc != 0:
         raise ValueError("oracle_accept_stochastic rejected its input (rc=%d)" % rc)
-    return a, nxt, mg
+    return a, nxt, ma, ms
+
+
+def successor_interval(logits, dtype, row, removed, temperature, token):
+    """Cumulative-probability interval ``(lo, hi)`` of ``token`` in the
+    successor distribution of packed row ``row`` (without ``removed``)."""
+    lib = _load()
+    lg, code = _logits_args(logits, dtype)
+    lo, hi = ctypes.c_double(0), ctypes.c_double(0)
+    rc = lib.oracle_successor_interval(_ptr(lg), code, int(row), lg.shape[1], int(removed),
+                                       float(temperature), int(token), ctypes.byref(lo),
+                                       ctypes.byref(hi))
+    if rc != 0:
+        raise ValueError("oracle_successor_interval rejected its input (rc=%d)" % rc)
+    return lo.value, hi.value

@@ -338,10 +338,12 @@ int oracle_dvl_pack(const int32_t *k_live, int32_t n, int32_t n_bs, int32_t w,
  * the smallest v whose cumulative probability exceeds u.  A candidate id
  * outside [0, vocab) has probability 0 and removes nothing.
  *
- * margin[i] (if not NULL) receives the smallest distance, in probability,
- * between one of the request's uniforms and the threshold its decision
- * compared it with (+inf for a sentinel): how far the result is from
- * flipping under a perturbation of the probabilities.
+ * margin_accept[i] and margin_sample[i] (each may be NULL) receive the
+ * smallest distance, in probability, between the request's accept-test
+ * uniforms and their thresholds P(x), and between its successor uniform and
+ * the nearest boundary of the cumulative distribution it inverts (+inf when
+ * there is no such decision): how far the result is from flipping under a
+ * perturbation of the probabilities.
  * ---------------------------------------------------------------------- */
 
 /* P(v) for one row: writes prob[0..vocab) (double), returns 0. */
@@ -364,8 +366,8 @@ int oracle_accept_stochastic(const void *logits, int32_t dtype,
                              const int32_t *cu_qlens, const int32_t *draft_tokens,
                              const float *uniforms, double temperature,
                              int32_t *accept_len, int32_t *next_token,
-                             double *margin, int32_t num_reqs, int32_t cap,
-                             int32_t vocab) {
+                             double *margin_accept, double *margin_sample,
+                             int32_t num_reqs, int32_t cap, int32_t vocab) {
   if (!logits || !cu_qlens || !draft_tokens || !uniforms || !accept_len || !next_token)
     return -1;
   if (num_reqs < 1 || cap < 1 || vocab < 1 || (dtype != 0 && dtype != 1)) return -1;
@@ -379,11 +381,12 @@ int oracle_accept_stochastic(const void *logits, int32_t dtype,
   for (int32_t i = 0; i < num_reqs; ++i) {
     int32_t o = cu_qlens[i];
     int32_t k = cu_qlens[i + 1] - o;
-    double mg = INFINITY;
+    double mg = INFINITY, ms = INFINITY;
     if (k == 0) {
       accept_len[i] = 0;
       next_token[i] = -1;
-      if (margin) margin[i] = mg;
+      if (margin_accept) margin_accept[i] = mg;
+      if (margin_sample) margin_sample[i] = ms;
       continue;
     }
     /* accept candidates while the uniform falls below their probability */
@@ -419,15 +422,37 @@ int oracle_accept_stochastic(const void *logits, int32_t dtype,
       last = v;
       if (pick < 0 && cum > us) {
         pick = v;
-        double d = us - before < cum - us ? us - before : cum - us;
-        if (d < mg) mg = d;
+        ms = us - before < cum - us ? us - before : cum - us;
       }
     }
     if (pick < 0) pick = last; /* u at or past the rounded total */
     accept_len[i] = a;
     next_token[i] = pick;
-    if (margin) margin[i] = mg;
+    if (margin_accept) margin_accept[i] = mg;
+    if (margin_sample) margin_sample[i] = ms;
   }
+  free(prob);
+  return 0;
+}
+
+int oracle_successor_interval(const void *logits, int32_t dtype, int32_t row,
+                              int32_t vocab, int32_t removed, double temperature,
+                              int32_t token, double *lo, double *hi) {
+  if (!logits || !lo || !hi || row < 0 || vocab < 1 || token < 0 || token >= vocab)
+    return -1;
+  if (!(temperature > 0.0) || !isfinite(temperature) || (dtype != 0 && dtype != 1)) return -1;
+  double *prob = (double *)malloc(sizeof(double) * (size_t)vocab);
+  if (!prob) return -1;
+  row_softmax(logits, dtype, (int64_t)row * vocab, vocab, 1.0 / temperature, prob);
+  double total = 1.0;
+  if (removed >= 0 && removed < vocab) {
+    total -= prob[removed];
+    prob[removed] = 0.0;
+  }
+  double cum = 0.0;
+  for (int32_t v = 0; v < token; ++v) cum += prob[v] / total;
+  *lo = cum;
+  *hi = cum + prob[token] / total;
   free(prob);
   return 0;
 }

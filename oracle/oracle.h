@@ -38,14 +38,23 @@ int oracle_accept(const void *logits, int32_t dtype, const int32_t *cu_qlens,
  * accepted iff uniforms[o+j][0] < P_{o+j}(x_j); the successor is drawn by
  * inverting the cumulative distribution (index order) of P_{o+a}, without
  * the rejected candidate if there is one, at uniforms[o+a][1].  uniforms is
- * float [cap][2].  margin (nullable) receives per request the smallest
- * distance between a uniform and the threshold it was compared with. */
+ * float [cap][2].  margin_accept / margin_sample (nullable) receive per
+ * request the smallest distance between a uniform and the threshold it was
+ * compared with, for the accept tests and for the successor draw. */
 int oracle_accept_stochastic(const void *logits, int32_t dtype,
                              const int32_t *cu_qlens, const int32_t *draft_tokens,
                              const float *uniforms, double temperature,
                              int32_t *accept_len, int32_t *next_token,
-                             double *margin, int32_t num_reqs, int32_t cap,
-                             int32_t vocab);
+                             double *margin_accept, double *margin_sample,
+                             int32_t num_reqs, int32_t cap, int32_t vocab);
+
+/* The interval [lo, hi) of cumulative probability (vocabulary order) that
+ * token `token` occupies in the successor distribution of packed row `row`:
+ * P = softmax(logits[row] / T), without token `removed` (-1: none),
+ * renormalised. */
+int oracle_successor_interval(const void *logits, int32_t dtype, int32_t row,
+                              int32_t vocab, int32_t removed, double temperature,
+                              int32_t token, double *lo, double *hi);
 
 /* ---- DVL budget allocation and flat-buffer packing (Sec. III-C) ----
  *

@@ -33,6 +33,8 @@ from ._lib import (  # noqa: F401
     Graph,
     KernelTimer,
     accept,
+    accept_stochastic,
+    accept_stochastic_workspace_bytes,
     accept_workspace_bytes,
     alloc_workspace,
     attn_dims,

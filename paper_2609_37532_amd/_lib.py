@@ -19,7 +19,8 @@ DSV_F32 = 0
 DSV_BF16 = 1
 MAX_QLEN = 16
 PAGE_SIZE = 16
-TIMING_KINDS = ("attn_split", "attn_combine", "accept_argmax", "accept_prefix", "dvl")
+TIMING_KINDS = ("attn_split", "attn_combine", "accept_argmax", "accept_prefix", "dvl",
+                "sample_stats", "sample_draw")
 DVL_MAX_REQS = 1024
 
 
@@ -61,6 +62,9 @@ def load():
         "dsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
         "dsv_accept": (ctypes.c_int, [P, I32, P, P, P, P, I32, I32, I32, P, SZ, P]),
         "dsv_validate_metadata": (ctypes.c_int, [P, P, P, PD, P, P]),
+        "dsv_accept_stochastic_workspace_bytes": (SZ, [I32, I32, I32]),
+        "dsv_accept_stochastic": (ctypes.c_int, [P, I32, P, P, P, ctypes.c_float, P, P, I32,
+                                                 I32, I32, P, SZ, P]),
         "dsv_dvl_allocate_pack": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P, P, I32, I32, P]),
         "dsv_graph_capture_begin": (ctypes.c_int, [P]),
         "dsv_graph_capture_end": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_void_p)]),
@@ -199,6 +203,37 @@ def accept(logits_packed, cu_qlens, draft_tokens, accept_len, next_token, *,
     _check("dsv_accept", load().dsv_accept(
         _ptr(logits_packed), dtype, _ptr(cu_qlens), _ptr(draft_tokens), _ptr(accept_len),
         _ptr(next_token), B, cap, vocab, _ptr(workspace), nbytes, _stream_handle(stream)))
+
+
+def accept_stochastic_workspace_bytes(capacity: int, num_reqs: int, vocab: int) -> int:
+    return int(load().dsv_accept_stochastic_workspace_bytes(capacity, num_reqs, vocab))
+
+
+def accept_stochastic(logits_packed, cu_qlens, draft_tokens, uniforms, temperature: float,
+                      accept_len, next_token, *, workspace=None, stream=None) -> None:
+    """Enqueue ``dsv_accept_stochastic`` (temperature > 0); ``uniforms`` is a
+    float32 [cap, 2] device tensor of values in [0, 1)."""
+    import torch
+    _require(logits_packed, "logits_packed", (torch.float32, torch.bfloat16), 2)
+    _require(uniforms, "uniforms", (torch.float32,), 2)
+    for t, n in ((cu_qlens, "cu_qlens"), (draft_tokens, "draft_tokens"),
+                 (accept_len, "accept_len"), (next_token, "next_token")):
+        _require(t, n, (torch.int32,), 1)
+    cap, vocab = logits_packed.shape
+    B = cu_qlens.numel() - 1
+    if draft_tokens.numel() != cap or accept_len.numel() != B or next_token.numel() != B:
+        raise ValueError("draft_tokens must be [cap]; accept_len, next_token [B]")
+    if tuple(uniforms.shape) != (cap, 2):
+        raise ValueError("uniforms must be [cap, 2]")
+    dtype = DSV_BF16 if logits_packed.dtype == torch.bfloat16 else DSV_F32
+    if workspace is None:
+        workspace = alloc_workspace(accept_stochastic_workspace_bytes(cap, B, vocab),
+                                    logits_packed.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    _check("dsv_accept_stochastic", load().dsv_accept_stochastic(
+        _ptr(logits_packed), dtype, _ptr(cu_qlens), _ptr(draft_tokens), _ptr(uniforms),
+        float(temperature), _ptr(accept_len), _ptr(next_token), B, cap, vocab, _ptr(workspace),
+        nbytes, _stream_handle(stream)))
 
 
 def validate_metadata(cu_qlens, ctx_lens, page_table, dims: AttnDims, err_word,

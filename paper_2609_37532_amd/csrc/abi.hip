@@ -4,6 +4,8 @@
 
 #include <math.h>
 
+#include <cmath>
+
 using namespace dsv;
 
 namespace {
@@ -132,6 +134,37 @@ int dsv_accept(const void *logits_packed, int32_t dtype, const int32_t *cu_qlens
       num_reqs, capacity, vocab, (float *)((char *)workspace + ws.val_off),
       (int32_t *)((char *)workspace + ws.idx_off), ws.num_chunks,
       (hipStream_t)hip_stream);
+  return e == hipSuccess ? DSV_OK : DSV_ERR_HIP;
+}
+
+size_t dsv_accept_stochastic_workspace_bytes(int32_t capacity, int32_t num_reqs,
+                                             int32_t vocab) {
+  if (capacity < 1 || num_reqs < 1 || vocab < 1) return 0;
+  return sample_workspace_layout(capacity, vocab).total;
+}
+
+int dsv_accept_stochastic(const void *logits_packed, int32_t dtype, const int32_t *cu_qlens,
+                          const int32_t *draft_tokens, const float *uniforms,
+                          float temperature, int32_t *accept_len, int32_t *next_token,
+                          int32_t num_reqs, int32_t capacity, int32_t vocab,
+                          void *workspace, size_t workspace_bytes, void *hip_stream) {
+  if (!logits_packed || !cu_qlens || !draft_tokens || !uniforms || !accept_len ||
+      !next_token)
+    return DSV_ERR_NULL;
+  if (num_reqs < 1 || capacity < 1 || vocab < 1 || capacity > 65535 ||
+      num_reqs > (1 << 30))
+    return DSV_ERR_DIMS;
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return DSV_ERR_DIMS;
+  const float scale_log2 = (float)(1.4426950408889634 / (double)temperature);
+  if (!std::isfinite(scale_log2)) return DSV_ERR_DIMS;
+  if (dtype != DSV_F32 && dtype != DSV_BF16) return DSV_ERR_UNSUPPORTED;
+  const SampleWorkspace ws = sample_workspace_layout(capacity, vocab);
+  if (!workspace || !aligned256(workspace) || workspace_bytes < ws.total)
+    return DSV_ERR_WORKSPACE;
+  const hipError_t e = launch_accept_stochastic(
+      logits_packed, dtype, cu_qlens, draft_tokens, uniforms, scale_log2, accept_len,
+      next_token, num_reqs, capacity, vocab, (float *)((char *)workspace + ws.m_off),
+      (float *)((char *)workspace + ws.s_off), ws.num_chunks, (hipStream_t)hip_stream);
   return e == hipSuccess ? DSV_OK : DSV_ERR_HIP;
 }
 

@@ -68,6 +68,21 @@ hipError_t launch_validate(const int32_t *cu, const int32_t *ctx,
                            int32_t *err_word, hipStream_t s);
 
 // -------------------------------------------------------------------------
+// stochastic acceptance (temperature > 0)
+// -------------------------------------------------------------------------
+struct SampleWorkspace {
+  size_t m_off, s_off, total;
+  int32_t num_chunks;
+};
+SampleWorkspace sample_workspace_layout(int32_t cap, int32_t vocab);
+hipError_t launch_accept_stochastic(const void *logits, int dtype, const int32_t *cu,
+                                    const int32_t *draft, const float *uniforms,
+                                    float scale_log2, int32_t *accept_len,
+                                    int32_t *next_token, int32_t num_reqs, int32_t cap,
+                                    int32_t vocab, float *stat_m, float *stat_s,
+                                    int32_t num_chunks, hipStream_t s);
+
+// -------------------------------------------------------------------------
 // DVL allocation and packing
 // -------------------------------------------------------------------------
 hipError_t launch_dvl(const float *pred_logits, const int32_t *num_live,
@@ -82,7 +97,9 @@ enum TimingKind {
   kTimeAttnCombine = 1,
   kTimeArgmax = 2,
   kTimePrefix = 3,
-  kTimeDvl = 4
+  kTimeDvl = 4,
+  kTimeSampleStats = 5,
+  kTimeSampleDraw = 6
 };
 // Records a HIP event before (end = false) or after (end = true) a launch
 // when timing is on and the stream is not being captured.

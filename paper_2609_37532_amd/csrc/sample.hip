@@ -1,0 +1,385 @@
+// sample.hip -- stochastic prefix verifier (temperature T > 0) for gfx950.
+//
+// What it computes (Sec. III-D "Prefix verifier"): the target policy at a
+// packed row is P = softmax(logits / T).  Request i's candidates are tested
+// in order; candidate x_j = draft[o+j+1] is accepted with probability
+// P_{o+j}(x_j), decided by the caller's uniform (accepted iff
+// u[o+j][0] < P(x)).  At the first rejection (row o+a) the successor is drawn
+// from P_{o+a} with x_a removed and the rest renormalised; if every
+// candidate passes, from P_{o+k-1} unchanged.  The draw inverts the
+// cumulative distribution in vocabulary order at u[o+a][1].
+//
+// How: the logits stream is the cost, as for the greedy verifier.  A first
+// kernel runs on (vocabulary chunk x live row) workgroups and writes, per
+// chunk, the maximum of the scaled logits and the sum of exp2 of their
+// differences to it (base-2 exponent with log2(e)/T folded into one
+// multiplier).  A second kernel, one workgroup per request, merges those
+// pairs into each row's normaliser in chunk order, makes the accept
+// decisions from single logit loads, then finds the successor: the chunk
+// holding the target mass from the chunk totals, and the token inside it
+// with one pass over that chunk and a block scan.  Everything is fp32 and
+// deterministic; the decisions agree with exact arithmetic except when a
+// uniform lies within rounding of its threshold.
+#include "dsv_internal.h"
+
+#include <math.h>
+
+namespace dsv {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kPerThread = kAcceptChunk / kThreads;  // successor-chunk elements per thread
+
+template <bool kBf16>
+__device__ __forceinline__ float elem(const void *row, int v) {
+  if (kBf16) return __uint_as_float((uint32_t)((const uint16_t *)row)[v] << 16);
+  return ((const float *)row)[v];
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// A logit times log2(e)/T, rounded on its own: never fused into a following
+// subtraction (a fused multiply-add would skip the product's rounding), so
+// every kernel -- and the row maximum -- sees the same value.
+__device__ __forceinline__ float scaled(float x, float c) {
+#pragma clang fp contract(off)
+  return x * c;
+}
+
+// Online (max, sum of exp2(y - max)) accumulation of one scaled value.
+__device__ __forceinline__ void acc(float &m, float &s, float y) {
+  if (y > m) {
+    s = s * exp2f(m - y) + 1.f;
+    m = y;
+  } else if (y > -INFINITY) {  // a -inf logit adds nothing
+    s += exp2f(y - m);
+  }
+}
+
+__device__ __forceinline__ void merge(float &m, float &s, float om, float os) {
+  if (om > m) {
+    s = s * exp2f(m - om) + os;
+    m = om;
+  } else if (om != -INFINITY) {
+    s += os * exp2f(om - m);
+  }
+}
+
+template <bool kBf16>
+__device__ __forceinline__ void acc_vec(u32x4 x, float c, float &m, float &s) {
+  if (kBf16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc(m, s, scaled(bf16_lo(x[q]), c));
+      acc(m, s, scaled(bf16_hi(x[q]), c));
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc(m, s, scaled(__uint_as_float(x[q]), c));
+  }
+}
+
+// Per (chunk, live row): max of logits * c and sum of exp2(logits * c - max).
+template <bool kBf16>
+__global__ __launch_bounds__(kThreads) void softmax_stats_kernel(
+    const void *logits, const int32_t *cu, int32_t num_reqs, int32_t cap, int32_t vocab,
+    int32_t num_chunks, float c, float *stat_m, float *stat_s) {
+  constexpr int kEs = kBf16 ? 2 : 4;
+  constexpr int kVec = 16 / kEs;
+  constexpr int kUnroll = kAcceptChunk / (kThreads * kVec);
+  const int ch = blockIdx.x, r = blockIdx.y;
+  const int live = min(cu[num_reqs], cap);
+  if (r >= live) return;
+  const char *row = (const char *)logits + (size_t)r * vocab * kEs;
+  const int begin = ch * kAcceptChunk;
+  const int end = min(vocab, begin + kAcceptChunk);
+  float m = -INFINITY, s = 0.f;
+  const uintptr_t addr = (uintptr_t)(row + (size_t)begin * kEs);
+  const int head = min(end - begin, (int)(((16 - (addr & 15)) & 15) / kEs));
+  const int vb = begin + head;
+  const int nvec = (end - vb) / kVec;
+  const int ve = vb + nvec * kVec;
+  const int tid = threadIdx.x;
+  if (tid < head) acc(m, s, scaled(elem<kBf16>(row, begin + tid), c));
+  if (tid < end - ve) acc(m, s, scaled(elem<kBf16>(row, ve + tid), c));
+  const u32x4 *vp = (const u32x4 *)(row + (size_t)vb * kEs);
+  if (nvec == kThreads * kUnroll) {
+    // full chunk: the values sit in registers, so take their maximum first
+    // and then one exponential each
+    u32x4 x[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) x[u] = __builtin_nontemporal_load(vp + u * kThreads + tid);
+    constexpr int kN = kUnroll * kVec;
+    float y[kN];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (kBf16) {
+          y[u * kVec + 2 * q] = scaled(bf16_lo(x[u][q]), c);
+          y[u * kVec + 2 * q + 1] = scaled(bf16_hi(x[u][q]), c);
+        } else {
+          y[u * kVec + q] = scaled(__uint_as_float(x[u][q]), c);
+        }
+      }
+    }
+    float lm = y[0];
+#pragma unroll
+    for (int q = 1; q < kN; ++q) lm = fmaxf(lm, y[q]);
+    float ls = 0.f;
+    if (lm > -INFINITY) {
+#pragma unroll
+      for (int q = 0; q < kN; ++q) ls += exp2f(y[q] - lm);
+    }
+    merge(m, s, lm, ls);
+  } else {
+    for (int q = tid; q < nvec; q += kThreads)
+      acc_vec<kBf16>(__builtin_nontemporal_load(vp + q), c, m, s);
+  }
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const float om = __shfl_xor(m, d, kWave);
+    const float os = __shfl_xor(s, d, kWave);
+    merge(m, s, om, os);
+  }
+  __shared__ float sm[kThreads / kWave], ss[kThreads / kWave];
+  const int wave = tid / kWave, lane = tid % kWave;
+  if (lane == 0) {
+    sm[wave] = m;
+    ss[wave] = s;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < kThreads / kWave; ++w) merge(m, s, sm[w], ss[w]);
+    stat_m[(size_t)r * num_chunks + ch] = m;
+    stat_s[(size_t)r * num_chunks + ch] = s;
+  }
+}
+
+// One workgroup per request: accept decisions, then the successor draw.
+template <bool kBf16>
+__global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
+    const void *logits, const int32_t *cu, const int32_t *draft, const float *uniforms,
+    int32_t *accept_len, int32_t *next_token, int32_t num_reqs, int32_t cap, int32_t vocab,
+    int32_t num_chunks, float c, const float *stat_m, const float *stat_s) {
+  constexpr int kEs = kBf16 ? 2 : 4;
+  __shared__ float s_rm[kMaxQlen], s_rz[kMaxQlen];
+  __shared__ int s_a;
+  __shared__ int s_chunk;
+  __shared__ float s_target;  // mass still to cover inside the chosen chunk
+  __shared__ float s_part[kThreads];
+  const int i = blockIdx.x, tid = threadIdx.x;
+  const int o = cu[i], k = cu[i + 1] - o;
+  if (k == 0) {
+    if (tid == 0) {
+      accept_len[i] = 0;
+      next_token[i] = -1;
+    }
+    return;
+  }
+  if (k < 0 || k > kMaxQlen || o < 0 || o + k > cap) return;  // bad metadata
+
+  // row normalisers: 16 lanes per row merge that row's chunk pairs in order
+  {
+    const int j = tid / 16, l = tid % 16;
+    float m = -INFINITY, s = 0.f;
+    if (j < k) {
+      const size_t base = (size_t)(o + j) * num_chunks;
+      for (int ch = l; ch < num_chunks; ch += 16) merge(m, s, stat_m[base + ch], stat_s[base + ch]);
+    }
+#pragma unroll
+    for (int d = 8; d >= 1; d >>= 1) {
+      const float om = __shfl_xor(m, d, 16);
+      const float os = __shfl_xor(s, d, 16);
+      merge(m, s, om, os);
+    }
+    if (j < k && l == 0) {
+      s_rm[j] = m;
+      s_rz[j] = s;
+    }
+  }
+  __syncthreads();
+
+  // accept decisions: wave 0, lane j tests candidate j
+  if (tid < kWave) {
+    bool reject = false;
+    if (tid < k - 1) {
+      const int x = draft[o + tid + 1];
+      float p = 0.f;
+      if (x >= 0 && x < vocab) {
+        const char *row = (const char *)logits + (size_t)(o + tid) * vocab * kEs;
+        p = exp2f(scaled(elem<kBf16>(row, x), c) - s_rm[tid]) / s_rz[tid];
+      }
+      reject = !(uniforms[2 * (size_t)(o + tid)] < p);
+    }
+    const unsigned long long mask = __ballot(reject);
+    if (tid == 0) s_a = mask ? __builtin_ctzll(mask) : k - 1;
+  }
+  __syncthreads();
+  const int a = s_a;
+  const int r = o + a;
+  const char *row = (const char *)logits + (size_t)r * vocab * kEs;
+  const float M = s_rm[a];
+  int removed = -1;
+  if (a < k - 1) {
+    const int x = draft[r + 1];
+    removed = (x >= 0 && x < vocab) ? x : -1;
+  }
+  const float ex = removed >= 0 ? exp2f(scaled(elem<kBf16>(row, removed), c) - M) : 0.f;
+
+  // the chunk holding the target mass (one thread, chunk order)
+  __shared__ int s_alt;  // last chunk with mass other than the removed token's
+  if (tid == 0) {
+    const size_t base = (size_t)r * num_chunks;
+    const int rc = removed >= 0 ? removed / kAcceptChunk : -1;
+    const float total = s_rz[a] - ex;
+    const float t = uniforms[2 * (size_t)r + 1] * total;
+    float cum = 0.f;
+    int pick = -1, last = -1, alt = -1;
+    float pick_rest = 0.f, last_w = 0.f;
+    for (int ch = 0; ch < num_chunks; ++ch) {
+      const float sm = stat_m[base + ch];
+      float w = sm == -INFINITY ? 0.f : stat_s[base + ch] * exp2f(sm - M);
+      if (ch == rc) w = fmaxf(w - ex, 0.f);
+      else if (w > 0.f) alt = ch;
+      if (w > 0.f) {
+        last = ch;
+        last_w = w;
+      }
+      if (pick < 0 && w > 0.f && cum + w > t) {
+        pick = ch;
+        pick_rest = t - cum;
+      }
+      cum += w;
+    }
+    if (pick < 0) {  // the uniform at or past the rounded total
+      pick = last >= 0 ? last : 0;
+      pick_rest = last_w;
+    }
+    s_chunk = pick;
+    s_target = pick_rest;
+    s_alt = alt;
+  }
+  __syncthreads();
+
+  // Inside the chunk: per-thread masses of 32 consecutive tokens, then the
+  // thread whose range covers the target, then the token.  If rounding left
+  // the chosen chunk without mass (only possible for the chunk that held
+  // the removed candidate), the last other chunk with mass is used instead,
+  // at its end.
+  __shared__ int s_who;
+  for (int attempt = 0; attempt < 2; ++attempt) {
+    const int ch = s_chunk;
+    const int v0 = ch * kAcceptChunk + tid * kPerThread;
+    float e[kPerThread];
+    float mine = 0.f;
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+      const int v = v0 + q;
+      float ev = 0.f;
+      if (v < vocab && v != removed) ev = exp2f(scaled(elem<kBf16>(row, v), c) - M);
+      e[q] = ev;
+      mine += ev;
+    }
+    s_part[tid] = mine;
+    __syncthreads();
+    if (tid == 0) {
+      const float t = s_target;
+      float cum = 0.f;
+      int who = -1, last = -1;
+      float rest = 0.f, last_rest = 0.f;
+      for (int q = 0; q < kThreads; ++q) {
+        const float w = s_part[q];
+        if (w > 0.f) {
+          last = q;
+          last_rest = w;
+        }
+        if (who < 0 && w > 0.f && cum + w > t) {
+          who = q;
+          rest = t - cum;
+        }
+        cum += w;
+      }
+      if (who < 0) {
+        who = last;
+        rest = last_rest;
+      }
+      s_who = who;
+      s_target = rest;
+      if (who < 0) {  // no mass here: retry at the end of another chunk
+        s_chunk = s_alt >= 0 ? s_alt : ch;
+        s_target = INFINITY;
+      }
+    }
+    __syncthreads();
+    const int who = s_who;
+    if (who >= 0) {
+      if (tid == who) {
+        const float t = s_target;
+        float cum = 0.f;
+        int pick = -1, last = -1;
+#pragma unroll
+        for (int q = 0; q < kPerThread; ++q) {
+          if (e[q] > 0.f) {
+            last = v0 + q;
+            if (pick < 0 && cum + e[q] > t) pick = v0 + q;
+          }
+          cum += e[q];
+        }
+        accept_len[i] = a;
+        next_token[i] = pick >= 0 ? pick : last;
+      }
+      return;
+    }
+    if (attempt == 1 || s_alt < 0) break;
+  }
+  // every token but the rejected one has zero probability in fp32: emit the
+  // rejected candidate (its renormalised distribution is undefined)
+  if (tid == 0) {
+    accept_len[i] = a;
+    next_token[i] = removed >= 0 ? removed : 0;
+  }
+}
+
+}  // namespace
+
+SampleWorkspace sample_workspace_layout(int32_t cap, int32_t vocab) {
+  SampleWorkspace w;
+  w.num_chunks = (vocab + kAcceptChunk - 1) / kAcceptChunk;
+  const size_t n = (size_t)cap * w.num_chunks;
+  w.m_off = 0;
+  w.s_off = align_up(n * sizeof(float), 256);
+  w.total = align_up(w.s_off + n * sizeof(float), 256);
+  return w;
+}
+
+hipError_t launch_accept_stochastic(const void *logits, int dtype, const int32_t *cu,
+                                    const int32_t *draft, const float *uniforms,
+                                    float scale_log2, int32_t *accept_len,
+                                    int32_t *next_token, int32_t num_reqs, int32_t cap,
+                                    int32_t vocab, float *stat_m, float *stat_s,
+                                    int32_t num_chunks, hipStream_t s) {
+  const dim3 grid(num_chunks, cap);
+  timing_mark(kTimeSampleStats, false, s);
+  if (dtype == DSV_BF16)
+    hipLaunchKernelGGL(softmax_stats_kernel<true>, grid, dim3(kThreads), 0, s, logits, cu,
+                       num_reqs, cap, vocab, num_chunks, scale_log2, stat_m, stat_s);
+  else
+    hipLaunchKernelGGL(softmax_stats_kernel<false>, grid, dim3(kThreads), 0, s, logits, cu,
+                       num_reqs, cap, vocab, num_chunks, scale_log2, stat_m, stat_s);
+  timing_mark(kTimeSampleStats, true, s);
+  timing_mark(kTimeSampleDraw, false, s);
+  if (dtype == DSV_BF16)
+    hipLaunchKernelGGL(stochastic_prefix_kernel<true>, dim3(num_reqs), dim3(kThreads), 0, s,
+                       logits, cu, draft, uniforms, accept_len, next_token, num_reqs, cap,
+                       vocab, num_chunks, scale_log2, stat_m, stat_s);
+  else
+    hipLaunchKernelGGL(stochastic_prefix_kernel<false>, dim3(num_reqs), dim3(kThreads), 0, s,
+                       logits, cu, draft, uniforms, accept_len, next_token, num_reqs, cap,
+                       vocab, num_chunks, scale_log2, stat_m, stat_s);
+  timing_mark(kTimeSampleDraw, true, s);
+  return hipGetLastError();
+}
+
+}  // namespace dsv

@@ -160,3 +160,20 @@ def test_dvl_rejects_bad_arguments():
     for w in (0, 1, 3, 15, 18):
         bad = list(args); bad[12] = w
         assert lib.dsv_dvl_allocate_pack(*bad) == -2
+
+
+def test_accept_stochastic_rejects_bad_arguments():
+    lib = dsv.load()
+    fake = 1 << 20
+    need = lib.dsv_accept_stochastic_workspace_bytes(256, 32, 151936)
+    assert need > 0 and need % 256 == 0
+    args = [fake, 1, fake, fake, fake, 1.0, fake, fake, 32, 256, 151936, fake, need, None]
+    bad = list(args); bad[4] = None
+    assert lib.dsv_accept_stochastic(*bad) == -1
+    for t in (0.0, -1.0, float("inf"), float("nan"), 1e-45):
+        bad = list(args); bad[5] = t
+        assert lib.dsv_accept_stochastic(*bad) == -2, t
+    bad = list(args); bad[1] = 3
+    assert lib.dsv_accept_stochastic(*bad) == -3
+    bad = list(args); bad[12] = need - 1
+    assert lib.dsv_accept_stochastic(*bad) == -4

@@ -31,9 +31,12 @@ def test_hand_example():
              ((0.6, 0.9), (0, 1))]
     for (u0, us), (a_want, t_want) in cases:
         U = np.array([[u0, us], [0.5, us]], np.float32)
-        a, t, mg = oracle.accept_stochastic(L, "f32", cu, draft, U, 1.0)
+        a, t, ma, ms = oracle.accept_stochastic(L, "f32", cu, draft, U, 1.0)
         assert (int(a[0]), int(t[0])) == (a_want, t_want), (u0, us)
-        assert mg[0] > 0.05
+        assert ma[0] >= 0.1 - 1e-7 and ms[0] > 0.05
+        lo, hi = oracle.successor_interval(L, "f32", int(a[0]),
+                                           2 if a_want == 0 else -1, 1.0, int(t[0]))
+        assert lo <= us < hi
 
 
 def batch(rng, n, rows_logits, draft_block, T, dtype="f32"):
@@ -43,7 +46,7 @@ def batch(rng, n, rows_logits, draft_block, T, dtype="f32"):
     cu = (np.arange(n + 1) * k).astype(np.int32)
     draft = np.tile(draft_block, n).astype(np.int32)
     U = rng.random((n * k, 2)).astype(np.float32)
-    a, t, _ = oracle.accept_stochastic(logits, dtype, cu, draft, U, T)
+    a, t, _, _ = oracle.accept_stochastic(logits, dtype, cu, draft, U, T)
     return a, t
 
 
@@ -102,7 +105,7 @@ def test_low_temperature_is_greedy():
     follow = rng.random(cap) < 0.7          # drafts that copy the previous row's argmax
     draft[1:][follow[1:]] = top[:-1][follow[1:]]
     U = rng.uniform(0.001, 0.999, size=(cap, 2)).astype(np.float32)
-    a, t, _ = oracle.accept_stochastic(logits, "f32", cu, draft, U, 1e-3)
+    a, t, _, _ = oracle.accept_stochastic(logits, "f32", cu, draft, U, 1e-3)
     ga, gt = oracle.accept(logits, "f32", cu, draft)
     assert np.array_equal(a, ga) and np.array_equal(t, gt)
 
@@ -114,9 +117,9 @@ def test_sentinels_single_rows_and_bad_ids():
     cu = np.array([0, 0, 1, 3, 3, 6], np.int32)  # sentinel, k=1, k=2, sentinel, k=3
     draft = np.array([1, 2, -5, 4, 4, V + 3], np.int32)  # rows 2 and 5 hold invalid ids
     U = np.full((6, 2), 0.0, np.float32)   # u = 0 accepts any candidate with P > 0
-    a, t, mg = oracle.accept_stochastic(logits, "f32", cu, draft, U, 1.0)
+    a, t, ma, ms = oracle.accept_stochastic(logits, "f32", cu, draft, U, 1.0)
     assert (a[0], t[0]) == (0, -1) and (a[3], t[3]) == (0, -1)
-    assert np.isinf(mg[0]) and np.isinf(mg[3])
+    assert np.isinf(ma[0]) and np.isinf(ms[3]) and np.isinf(ma[1])
     assert a[1] == 0 and t[1] == 0          # k=1: u_s = 0 draws the first token
     assert a[2] == 0                         # candidate -5 has probability 0
     assert a[4] == 1                         # candidate 4 accepted, V+3 rejected
