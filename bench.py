@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--no-stress", action="store_true",
                     help="skip the 36-layer graph-replay stress measurement")
     ap.add_argument("--stress-steps", type=int, default=100)
+    ap.add_argument("--no-next", action="store_true",
+                    help="skip the next-row sections (stochastic verifier, DVL, bucket set)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only copy a 1 GiB device buffer three times: the plain copy "
                          "of known size that scales the hardware byte counters")
@@ -472,12 +474,46 @@ def main():
     }
     graph.close()
 
+    if args.no_next:
+        finish(args, result, attn, acc, torch)
+        return
+    # ---- the stochastic verifier (T = 1) on the same logits and offsets
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(W.SEED_BASE + 90)
+    uni = torch.rand((acc.capacity, 2), generator=gen, device=dev, dtype=torch.float32)
+    ws_smp = dsv.alloc_workspace(
+        dsv.accept_stochastic_workspace_bytes(acc.capacity, acc.num_reqs, acc.vocab), dev)
+    smp = lambda: dsv.accept_stochastic(logits, cu, draft, uni, 1.0, a_len, nxt,
+                                        workspace=ws_smp, stream=stream)
+    for _ in range(3):
+        smp()
+    torch.cuda.synchronize()
+    timer = dsv.KernelTimer(max_launches=2 * n_timed + 8)
+    with timer:
+        for _ in range(n_timed):
+            smp()
+        torch.cuda.synchronize()
+    t_stats = timer.mean_ms("sample_stats") * 1e-3
+    t_draw = timer.mean_ms("sample_draw") * 1e-3
+    s_gbps = b_acc / t_stats / 1e9
+    result["stochastic_accept"] = {
+        "temperature": 1.0, "stats_us": round(t_stats * 1e6, 2),
+        "draw_us": round(t_draw * 1e6, 2), "algorithmic_bytes": b_acc,
+        "stats_gbps": round(s_gbps, 1), "stats_frac": round(s_gbps / HBM_PEAK_GBPS, 4),
+        "timing": "HIP events around each launch, %d launches" % n_timed}
+
     del q, kv, logits, out
     torch.cuda.empty_cache()
     log("DVL allocate-and-pack ...")
     result["dvl"] = dvl_bench()
     log("bucket set ...")
     result["buckets"] = bucket_bench()
+    finish(args, result, attn, acc, torch)
+
+
+def finish(args, result, attn, acc, torch):
+    """The stress run and the CPU baseline, then the JSON line."""
+    torch.cuda.empty_cache()
     if not args.no_stress:
         log("stress run (36 layers, %d steps) ..." % args.stress_steps)
         result["stress"] = stress_bench(args.stress_steps)

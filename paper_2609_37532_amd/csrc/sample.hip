@@ -47,6 +47,24 @@ __device__ __forceinline__ float scaled(float x, float c) {
   return x * c;
 }
 
+// Inclusive prefix sum of floats over the 64 lanes of a wave (DPP row shifts,
+// then row broadcasts; lanes without a source add 0).  Adding non-negative
+// values keeps the prefix non-decreasing, lane by lane.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_add(float v) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, kRowMask, 0xf, false));
+}
+__device__ __forceinline__ float wave_incl_scan_f(float v) {
+  v += dpp_add<0x111, 0xf>(v);  // row_shr:1
+  v += dpp_add<0x112, 0xf>(v);  // row_shr:2
+  v += dpp_add<0x114, 0xf>(v);  // row_shr:4
+  v += dpp_add<0x118, 0xf>(v);  // row_shr:8
+  v += dpp_add<0x142, 0xa>(v);  // row_bcast:15
+  v += dpp_add<0x143, 0xc>(v);  // row_bcast:31
+  return v;
+}
+
 // Online (max, sum of exp2(y - max)) accumulation of one scaled value.
 __device__ __forceinline__ void acc(float &m, float &s, float y) {
   if (y > m) {
@@ -168,7 +186,7 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
   __shared__ int s_a;
   __shared__ int s_chunk;
   __shared__ float s_target;  // mass still to cover inside the chosen chunk
-  __shared__ float s_part[kThreads];
+  __shared__ float s_part[kThreads];  // inclusive token-order sums per thread
   const int i = blockIdx.x, tid = threadIdx.x;
   const int o = cu[i], k = cu[i + 1] - o;
   if (k == 0) {
@@ -228,49 +246,67 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
   }
   const float ex = removed >= 0 ? exp2f(scaled(elem<kBf16>(row, removed), c) - M) : 0.f;
 
-  // the chunk holding the target mass (one thread, chunk order)
+  // The chunk holding the target mass: wave 0 takes 64 chunks at a time,
+  // scans their masses in chunk order and picks the first chunk whose
+  // inclusive sum exceeds the target.
   __shared__ int s_alt;  // last chunk with mass other than the removed token's
-  if (tid == 0) {
+  if (tid < kWave) {
     const size_t base = (size_t)r * num_chunks;
     const int rc = removed >= 0 ? removed / kAcceptChunk : -1;
-    const float total = s_rz[a] - ex;
-    const float t = uniforms[2 * (size_t)r + 1] * total;
-    float cum = 0.f;
+    const float t = uniforms[2 * (size_t)r + 1] * (s_rz[a] - ex);
+    float carry = 0.f;
     int pick = -1, last = -1, alt = -1;
     float pick_rest = 0.f, last_w = 0.f;
-    for (int ch = 0; ch < num_chunks; ++ch) {
-      const float sm = stat_m[base + ch];
-      float w = sm == -INFINITY ? 0.f : stat_s[base + ch] * exp2f(sm - M);
-      if (ch == rc) w = fmaxf(w - ex, 0.f);
-      else if (w > 0.f) alt = ch;
-      if (w > 0.f) {
-        last = ch;
-        last_w = w;
+    for (int c0 = 0; c0 < num_chunks; c0 += kWave) {
+      const int ch = c0 + tid;
+      float w = 0.f;
+      if (ch < num_chunks) {
+        const float sm = stat_m[base + ch];
+        w = sm == -INFINITY ? 0.f : stat_s[base + ch] * exp2f(sm - M);
+        if (ch == rc) w = fmaxf(w - ex, 0.f);
       }
-      if (pick < 0 && w > 0.f && cum + w > t) {
-        pick = ch;
-        pick_rest = t - cum;
+      const float incl = carry + wave_incl_scan_f(w);
+      const unsigned long long pos = __ballot(w > 0.f);
+      const unsigned long long other = __ballot(w > 0.f && ch != rc);
+      if (pos) {
+        last = c0 + 63 - __builtin_clzll(pos);
+        last_w = __shfl(w, 63 - __builtin_clzll(pos), kWave);
       }
-      cum += w;
+      if (other) alt = c0 + 63 - __builtin_clzll(other);
+      const unsigned long long hit = __ballot(w > 0.f && incl > t);
+      if (pick < 0 && hit) {
+        const int l = __builtin_ctzll(hit);
+        const float before = l > 0 ? __shfl(incl, l - 1, kWave) : carry;
+        pick = c0 + l;
+        pick_rest = t - before;
+      }
+      carry = __shfl(incl, kWave - 1, kWave);
+      if (pick >= 0) break;  // uniform: every lane saw the same ballot
     }
     if (pick < 0) {  // the uniform at or past the rounded total
       pick = last >= 0 ? last : 0;
       pick_rest = last_w;
     }
-    s_chunk = pick;
-    s_target = pick_rest;
-    s_alt = alt;
+    if (tid == 0) {
+      s_chunk = pick;
+      s_target = pick_rest;
+      s_alt = alt;
+    }
   }
   __syncthreads();
 
-  // Inside the chunk: per-thread masses of 32 consecutive tokens, then the
-  // thread whose range covers the target, then the token.  If rounding left
+  // Inside the chunk: per-thread masses of 32 consecutive tokens, a block
+  // scan in token order, the first thread whose inclusive sum exceeds the
+  // target, then the token inside that thread's range.  If rounding left
   // the chosen chunk without mass (only possible for the chunk that held
   // the removed candidate), the last other chunk with mass is used instead,
   // at its end.
-  __shared__ int s_who;
+  __shared__ float s_wtot[kThreads / kWave];
+  __shared__ int s_whit[kThreads / kWave], s_wlast[kThreads / kWave];
+  const int wave = tid / kWave, lane = tid % kWave;
   for (int attempt = 0; attempt < 2; ++attempt) {
     const int ch = s_chunk;
+    const float t = s_target;
     const int v0 = ch * kAcceptChunk + tid * kPerThread;
     float e[kPerThread];
     float mine = 0.f;
@@ -282,57 +318,54 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
       e[q] = ev;
       mine += ev;
     }
-    s_part[tid] = mine;
+    float incl = wave_incl_scan_f(mine);
+    if (lane == kWave - 1) s_wtot[wave] = incl;
     __syncthreads();
-    if (tid == 0) {
-      const float t = s_target;
-      float cum = 0.f;
-      int who = -1, last = -1;
-      float rest = 0.f, last_rest = 0.f;
-      for (int q = 0; q < kThreads; ++q) {
-        const float w = s_part[q];
-        if (w > 0.f) {
-          last = q;
-          last_rest = w;
-        }
-        if (who < 0 && w > 0.f && cum + w > t) {
-          who = q;
-          rest = t - cum;
-        }
-        cum += w;
-      }
-      if (who < 0) {
-        who = last;
-        rest = last_rest;
-      }
-      s_who = who;
-      s_target = rest;
-      if (who < 0) {  // no mass here: retry at the end of another chunk
-        s_chunk = s_alt >= 0 ? s_alt : ch;
-        s_target = INFINITY;
-      }
+    for (int w = 0; w < wave; ++w) incl += s_wtot[w];
+    s_part[tid] = incl;
+    const unsigned long long hit = __ballot(mine > 0.f && incl > t);
+    const unsigned long long pos = __ballot(mine > 0.f);
+    if (lane == 0) {
+      s_whit[wave] = hit ? wave * kWave + __builtin_ctzll(hit) : -1;
+      s_wlast[wave] = pos ? wave * kWave + 63 - __builtin_clzll(pos) : -1;
     }
     __syncthreads();
-    const int who = s_who;
-    if (who >= 0) {
+    int who = -1, last = -1;
+    for (int w = 0; w < kThreads / kWave; ++w) {
+      if (who < 0) who = s_whit[w];
+      if (s_wlast[w] >= 0) last = s_wlast[w];
+    }
+    if (who >= 0 || last >= 0) {
+      const bool fallback = who < 0;
+      if (fallback) who = last;
       if (tid == who) {
-        const float t = s_target;
+        // mass before this thread's range, then the token
+        const float before = who > 0 ? s_part[who - 1] : 0.f;
+        const float rest = fallback ? mine : t - before;
         float cum = 0.f;
-        int pick = -1, last = -1;
+        int pick = -1, lastv = -1;
 #pragma unroll
         for (int q = 0; q < kPerThread; ++q) {
           if (e[q] > 0.f) {
-            last = v0 + q;
-            if (pick < 0 && cum + e[q] > t) pick = v0 + q;
+            lastv = v0 + q;
+            if (pick < 0 && cum + e[q] > rest) pick = v0 + q;
           }
           cum += e[q];
         }
         accept_len[i] = a;
-        next_token[i] = pick >= 0 ? pick : last;
+        next_token[i] = pick >= 0 ? pick : lastv;
       }
       return;
     }
-    if (attempt == 1 || s_alt < 0) break;
+    // no mass here: retry at the end of another chunk
+    const int alt = s_alt;
+    if (attempt == 1 || alt < 0) break;
+    __syncthreads();  // every thread has read s_chunk / s_target / s_part
+    if (tid == 0) {
+      s_chunk = alt;
+      s_target = INFINITY;
+    }
+    __syncthreads();
   }
   // every token but the rejected one has zero probability in fp32: emit the
   // rejected candidate (its renormalised distribution is undefined)
