@@ -62,7 +62,9 @@ def _load():
     lib.oracle_dvl_scores.argtypes = [p, i32, i32, p, p, p]
     lib.oracle_dvl_adjust.argtypes = [p, p, i32, i32, i32, p, p]
     lib.oracle_dvl_pack.argtypes = [p, i32, i32, i32, i32, p, p, p, p, p, p, p, p]
-    for f in (lib.oracle_dvl_scores, lib.oracle_dvl_adjust, lib.oracle_dvl_pack):
+    lib.oracle_predictor_forward.argtypes = [p, i32, i32, p, p, p, p, i32, i32, i32, p]
+    for f in (lib.oracle_dvl_scores, lib.oracle_dvl_adjust, lib.oracle_dvl_pack,
+              lib.oracle_predictor_forward):
         f.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -249,3 +251,20 @@ def successor_interval(logits, dtype, row, removed, temperature, token):
     if rc != 0:
         raise ValueError("oracle_successor_interval rejected its input (rc=%d)" % rc)
     return lo.value, hi.value
+
+
+def predictor_forward(features, n_live, w1, b1, w2, b2):
+    """Acceptance predictor forward (Eq. (5)) in float64: features [n, in],
+    W1 [in, hidden], W2 [hidden, out]; rows past ``n_live`` are zero."""
+    lib = _load()
+    f = _c(features, np.float32)
+    w1, b1, w2, b2 = (_c(x, np.float32) for x in (w1, b1, w2, b2))
+    n, in_dim = f.shape
+    hidden, out_dim = w2.shape
+    assert w1.shape == (in_dim, hidden) and b1.shape == (hidden,) and b2.shape == (out_dim,)
+    out = np.empty((n, out_dim), np.float64)
+    rc = lib.oracle_predictor_forward(_ptr(f), int(n_live), n, _ptr(w1), _ptr(b1), _ptr(w2),
+                                      _ptr(b2), in_dim, hidden, out_dim, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_predictor_forward rejected its input (rc=%d)" % rc)
+    return out

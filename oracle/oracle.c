@@ -456,3 +456,42 @@ int oracle_successor_interval(const void *logits, int32_t dtype, int32_t row,
   free(prob);
   return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Acceptance predictor forward (Sec. III-C, Eq. (5)): a multilayer
+ * perceptron with one ReLU hidden layer, in_dim -> hidden -> out_dim (the
+ * paper's 1735 -> 64 -> 15).  For each live request i:
+ *   h = max(0, features_i . W1 + b1),   predLogits_i = h . W2 + b2,
+ * with W1 [in_dim][hidden], W2 [hidden][out_dim] row-major, everything
+ * widened to double.  Rows past n_live get zeros.
+ * ---------------------------------------------------------------------- */
+int oracle_predictor_forward(const float *features, int32_t n_live, int32_t n_rows,
+                             const float *w1, const float *b1, const float *w2,
+                             const float *b2, int32_t in_dim, int32_t hidden,
+                             int32_t out_dim, double *out) {
+  if (!features || !w1 || !b1 || !w2 || !b2 || !out) return -1;
+  if (n_rows < 1 || n_live < 0 || n_live > n_rows || in_dim < 1 || hidden < 1 || out_dim < 1)
+    return -1;
+  double *h = (double *)malloc(sizeof(double) * (size_t)hidden);
+  if (!h) return -1;
+  for (int32_t i = 0; i < n_rows; ++i) {
+    double *o = out + (int64_t)i * out_dim;
+    if (i >= n_live) {
+      for (int32_t j = 0; j < out_dim; ++j) o[j] = 0.0;
+      continue;
+    }
+    const float *f = features + (int64_t)i * in_dim;
+    for (int32_t u = 0; u < hidden; ++u) {
+      double acc = (double)b1[u];
+      for (int32_t k = 0; k < in_dim; ++k) acc += (double)f[k] * (double)w1[(int64_t)k * hidden + u];
+      h[u] = acc > 0.0 ? acc : 0.0;
+    }
+    for (int32_t j = 0; j < out_dim; ++j) {
+      double acc = (double)b2[j];
+      for (int32_t u = 0; u < hidden; ++u) acc += h[u] * (double)w2[(int64_t)u * out_dim + j];
+      o[j] = acc;
+    }
+  }
+  free(h);
+  return 0;
+}

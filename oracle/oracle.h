@@ -56,6 +56,15 @@ int oracle_successor_interval(const void *logits, int32_t dtype, int32_t row,
                               int32_t vocab, int32_t removed, double temperature,
                               int32_t token, double *lo, double *hi);
 
+/* Acceptance predictor forward (Sec. III-C, Eq. (5)): per live row,
+ * h = relu(features . W1 + b1), out = h . W2 + b2, in double precision.
+ * features float [n_rows][in_dim]; W1 [in_dim][hidden]; W2 [hidden][out_dim];
+ * out double [n_rows][out_dim], zero past n_live. */
+int oracle_predictor_forward(const float *features, int32_t n_live, int32_t n_rows,
+                             const float *w1, const float *b1, const float *w2,
+                             const float *b2, int32_t in_dim, int32_t hidden,
+                             int32_t out_dim, double *out);
+
 /* ---- DVL budget allocation and flat-buffer packing (Sec. III-C) ----
  *
  * Decisions are taken in single precision, as the library takes them: each

@@ -31,4 +31,7 @@ from .gen import (  # noqa: F401
     DvlInputs,
     make_dvl_inputs,
     plant_boosts,
+    PREDICTOR_DIMS,
+    PredictorInputs,
+    make_predictor_inputs,
 )

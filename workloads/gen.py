@@ -551,3 +551,53 @@ def make_dvl_inputs(rng: np.random.Generator, *, n_bs: int, n_live: int,
         + positions % PAGE_SIZE
     return DvlInputs(pred_logits=logits, n_live=int(n_live), tokens=tokens,
                      positions=positions, kv_refs=kv_refs.astype(np.int32), width=w)
+
+
+# -------------------------------------------------------------- predictor
+PREDICTOR_DIMS = (1735, 64, 15)  # features, hidden units, draft positions
+
+
+@dataclass
+class PredictorInputs:
+    """Acceptance-predictor inputs for a bucket of ``n_bs`` slots (first
+    ``n_live`` live) and random weights of the 1735-64-15 shape.
+
+    Features follow the paper's layout: per draft position (15) the top
+    logit ~ N(14, 3), its 15 gaps to ranks 2..16 (sorted |N(0, 2)| partial
+    sums), the top token's log-probability -|N(0, 1)| and the entropy
+    U(0, 4) (270 values); 960 hidden-state projections ~ N(0, 1); 480 logit
+    projections ~ N(0, 1); a 25-value batch context with the live count
+    first, 1 in the fourth entry and zeros elsewhere.  Weights: W1 ~ N(0,
+    2/1735), b1 ~ N(0, 0.1), W2 ~ N(0, 1/64), b2 ~ N(1, 0.5) (the trained
+    weights are not available).  Sentinel feature rows are NaN."""
+    features: np.ndarray
+    n_live: int
+    w1: np.ndarray
+    b1: np.ndarray
+    w2: np.ndarray
+    b2: np.ndarray
+
+
+def make_predictor_inputs(rng: np.random.Generator, *, n_bs: int, n_live: int,
+                          dims=PREDICTOR_DIMS) -> PredictorInputs:
+    in_dim, hidden, out_dim = dims
+    f = np.zeros((n_bs, in_dim), np.float32)
+    pos = out_dim
+    if in_dim == 1735:
+        conf = np.zeros((n_bs, pos, 18), np.float32)
+        conf[:, :, 0] = rng.normal(14.0, 3.0, size=(n_bs, pos))
+        conf[:, :, 1:16] = np.cumsum(np.abs(rng.normal(0, 2.0, size=(n_bs, pos, 15))), axis=2)
+        conf[:, :, 16] = -np.abs(rng.normal(0, 1.0, size=(n_bs, pos)))
+        conf[:, :, 17] = rng.uniform(0, 4.0, size=(n_bs, pos))
+        f[:, :270] = conf.reshape(n_bs, 270)
+        f[:, 270:1710] = rng.normal(0, 1.0, size=(n_bs, 1440))
+        f[:, 1710] = n_live
+        f[:, 1713] = 1.0
+    else:
+        f[:] = rng.normal(0, 1.0, size=(n_bs, in_dim))
+    f[n_live:] = np.nan
+    w1 = rng.normal(0, np.sqrt(2.0 / in_dim), size=(in_dim, hidden)).astype(np.float32)
+    b1 = rng.normal(0, 0.1, size=hidden).astype(np.float32)
+    w2 = rng.normal(0, np.sqrt(1.0 / hidden), size=(hidden, out_dim)).astype(np.float32)
+    b2 = rng.normal(1.0, 0.5, size=out_dim).astype(np.float32)
+    return PredictorInputs(features=f, n_live=int(n_live), w1=w1, b1=b1, w2=w2, b2=b2)
