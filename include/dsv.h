@@ -16,6 +16,8 @@
  *   dsv_accept_stochastic
  *                    the same verifier at temperature > 0: probability-ratio
  *                    acceptance with residual resampling (Sec. III-D);
+ *   dsv_predictor_forward
+ *                    the acceptance predictor (Eq. (5)) that feeds DVL;
  *   dsv_dvl_allocate_pack
  *                    DVL budget allocation and flat-buffer packing (Sec.
  *                    III-C, Alg. 1, Eqs. (6)-(11)): per-request verify
@@ -257,6 +259,34 @@ int dsv_validate_metadata(const int32_t *cu_qlens, const int32_t *ctx_lens,
                           int32_t *err_word, void *hip_stream);
 
 /*
+ * Acceptance predictor forward (Sec. III-C, Eqs. (4)-(5)): for each live
+ * request i of a bucket of N_bs slots (the first N live, N read on the
+ * device and clamped into [0, N_bs]),
+ *   h = relu(features_i . W1 + b1),   pred_logits_i = h . W2 + b2,
+ * a perceptron with one ReLU hidden layer of DSV_PRED_HIDDEN units (the
+ * paper's 1735 -> 64 -> 15, 112,079 parameters).  Rows i >= N of
+ * pred_logits are written as 0; their features are not read.
+ *
+ *   features     fp32 [N_bs][in_dim], device.
+ *   W1 [in_dim][64], b1 [64], W2 [64][out_dim], b2 [out_dim]: fp32, row-major,
+ *                device.
+ *   pred_logits  fp32 [N_bs][out_dim], written; with out_dim = W-1 it is the
+ *                pred_logits input of dsv_dvl_allocate_pack.
+ *   hidden       must be DSV_PRED_HIDDEN (else DSV_ERR_UNSUPPORTED).
+ *   workspace    >= dsv_predictor_workspace_bytes(N_bs, in_dim) bytes,
+ *                256-byte aligned (per-slice partial sums; no zeroing needed).
+ * fp32 arithmetic in a fixed order: deterministic.  Host limits: 1 <= N_bs
+ * <= DSV_DVL_MAX_REQS, 1 <= in_dim <= 2^20, 1 <= out_dim <= 1024.
+ */
+#define DSV_PRED_HIDDEN 64
+size_t dsv_predictor_workspace_bytes(int32_t bucket_reqs, int32_t in_dim);
+int dsv_predictor_forward(const float *features, const int32_t *num_live, const float *w1,
+                          const float *b1, const float *w2, const float *b2,
+                          float *pred_logits, int32_t bucket_reqs, int32_t in_dim,
+                          int32_t hidden, int32_t out_dim, void *workspace,
+                          size_t workspace_bytes, void *hip_stream);
+
+/*
  * DVL budget allocation and flat-buffer packing (Sec. III-C, Alg. 1), for a
  * captured bucket of N_bs request slots of which the first N are live
  * (1 <= N <= N_bs; the rest are sentinels).  W = block_width (16 in the
@@ -337,17 +367,18 @@ int dsv_graph_destroy(void *graph_exec);
 /*
  * Kernel timing for measurement harnesses.  After dsv_timing_start(n), the
  * next n kernel launches made by eager (not captured) dsv_verify_attn,
- * dsv_accept, dsv_accept_stochastic and dsv_dvl_allocate_pack calls are
- * bracketed by HIP events
+ * dsv_accept, dsv_accept_stochastic, dsv_predictor_forward and
+ * dsv_dvl_allocate_pack calls are bracketed by HIP events
  * recorded on the caller's stream.  dsv_timing_stop waits for those events,
  * writes per kernel kind the summed milliseconds and the launch count (arrays
  * of DSV_TIMING_KINDS), and turns timing off.  Kinds: 0 attention split
  * kernel, 1 attention combine kernel, 2 vocabulary argmax kernel,
  * 3 prefix-compare kernel, 4 DVL allocate-and-pack kernel, 5 softmax
- * statistics kernel and 6 stochastic draw kernel of dsv_accept_stochastic.
+ * statistics kernel and 6 stochastic draw kernel of dsv_accept_stochastic,
+ * 7 the two predictor kernels of dsv_predictor_forward (one span).
  * Not thread-safe against concurrent calls from several host threads.
  */
-#define DSV_TIMING_KINDS 7
+#define DSV_TIMING_KINDS 8
 int dsv_timing_start(int32_t max_launches);
 int dsv_timing_stop(float *total_ms, int32_t *launches);
 

@@ -23,6 +23,7 @@ addresses; ``KernelTimer`` times the kernels with HIP events.
 from ._lib import (  # noqa: F401
     DSV_BF16,
     DVL_MAX_REQS,
+    PRED_HIDDEN,
     DSV_F32,
     LIB_PATH,
     MAX_QLEN,
@@ -39,6 +40,8 @@ from ._lib import (  # noqa: F401
     alloc_workspace,
     attn_dims,
     dvl_allocate_pack,
+    predictor_forward,
+    predictor_workspace_bytes,
     load,
     status_string,
     validate_metadata,

@@ -20,7 +20,8 @@ DSV_BF16 = 1
 MAX_QLEN = 16
 PAGE_SIZE = 16
 TIMING_KINDS = ("attn_split", "attn_combine", "accept_argmax", "accept_prefix", "dvl",
-                "sample_stats", "sample_draw")
+                "sample_stats", "sample_draw", "predictor")
+PRED_HIDDEN = 64
 DVL_MAX_REQS = 1024
 
 
@@ -65,6 +66,9 @@ def load():
         "dsv_accept_stochastic_workspace_bytes": (SZ, [I32, I32, I32]),
         "dsv_accept_stochastic": (ctypes.c_int, [P, I32, P, P, P, ctypes.c_float, P, P, I32,
                                                  I32, I32, P, SZ, P]),
+        "dsv_predictor_workspace_bytes": (SZ, [I32, I32]),
+        "dsv_predictor_forward": (ctypes.c_int, [P, P, P, P, P, P, P, I32, I32, I32, I32, P,
+                                                 SZ, P]),
         "dsv_dvl_allocate_pack": (ctypes.c_int, [P, P, P, P, P, P, P, P, P, P, P, I32, I32, P]),
         "dsv_graph_capture_begin": (ctypes.c_int, [P]),
         "dsv_graph_capture_end": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_void_p)]),
@@ -241,6 +245,39 @@ def validate_metadata(cu_qlens, ctx_lens, page_table, dims: AttnDims, err_word,
     _check("dsv_validate_metadata", load().dsv_validate_metadata(
         _ptr(cu_qlens), _ptr(ctx_lens), _ptr(page_table), ctypes.byref(dims),
         _ptr(err_word), _stream_handle(stream)))
+
+
+def predictor_workspace_bytes(bucket_reqs: int, in_dim: int) -> int:
+    return int(load().dsv_predictor_workspace_bytes(bucket_reqs, in_dim))
+
+
+def predictor_forward(features, num_live, w1, b1, w2, b2, pred_logits, *, workspace=None,
+                      stream=None) -> None:
+    """Enqueue ``dsv_predictor_forward`` (Eq. (5)): features float32
+    [N_bs, in_dim], W1 [in_dim, 64], b1 [64], W2 [64, out], b2 [out] ->
+    pred_logits float32 [N_bs, out]; ``num_live`` int32 [1] on the device."""
+    import torch
+    f32 = (torch.float32,)
+    _require(features, "features", f32, 2)
+    _require(w1, "w1", f32, 2)
+    _require(w2, "w2", f32, 2)
+    _require(b1, "b1", f32, 1)
+    _require(b2, "b2", f32, 1)
+    _require(pred_logits, "pred_logits", f32, 2)
+    _require(num_live, "num_live", (torch.int32,), 1)
+    n_bs, in_dim = features.shape
+    hidden, out_dim = w2.shape
+    if tuple(w1.shape) != (in_dim, hidden) or b1.numel() != hidden or b2.numel() != out_dim:
+        raise ValueError("weight shapes do not chain")
+    if tuple(pred_logits.shape) != (n_bs, out_dim) or num_live.numel() != 1:
+        raise ValueError("pred_logits must be [N_bs, out]; num_live one int32")
+    if workspace is None:
+        workspace = alloc_workspace(predictor_workspace_bytes(n_bs, in_dim), features.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    _check("dsv_predictor_forward", load().dsv_predictor_forward(
+        _ptr(features), _ptr(num_live), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
+        _ptr(pred_logits), n_bs, in_dim, hidden, out_dim, _ptr(workspace), nbytes,
+        _stream_handle(stream)))
 
 
 def dvl_allocate_pack(pred_logits, num_live, tokens, positions, kv_refs, k_out, cu_qlens,

@@ -179,6 +179,31 @@ int dsv_validate_metadata(const int32_t *cu_qlens, const int32_t *ctx_lens,
   return hipGetLastError() == hipSuccess ? DSV_OK : DSV_ERR_HIP;
 }
 
+size_t dsv_predictor_workspace_bytes(int32_t bucket_reqs, int32_t in_dim) {
+  if (bucket_reqs < 1 || bucket_reqs > DSV_DVL_MAX_REQS || in_dim < 1 || in_dim > (1 << 20))
+    return 0;
+  return predictor_workspace_bytes(bucket_reqs, in_dim);
+}
+
+int dsv_predictor_forward(const float *features, const int32_t *num_live, const float *w1,
+                          const float *b1, const float *w2, const float *b2,
+                          float *pred_logits, int32_t bucket_reqs, int32_t in_dim,
+                          int32_t hidden, int32_t out_dim, void *workspace,
+                          size_t workspace_bytes, void *hip_stream) {
+  if (!features || !num_live || !w1 || !b1 || !w2 || !b2 || !pred_logits) return DSV_ERR_NULL;
+  if (bucket_reqs < 1 || bucket_reqs > DSV_DVL_MAX_REQS || in_dim < 1 || in_dim > (1 << 20) ||
+      out_dim < 1 || out_dim > 1024)
+    return DSV_ERR_DIMS;
+  if (hidden != DSV_PRED_HIDDEN) return DSV_ERR_UNSUPPORTED;
+  if (!workspace || !aligned256(workspace) ||
+      workspace_bytes < predictor_workspace_bytes(bucket_reqs, in_dim))
+    return DSV_ERR_WORKSPACE;
+  const hipError_t e = launch_predictor(features, num_live, w1, b1, w2, b2, pred_logits,
+                                        bucket_reqs, in_dim, out_dim, (float *)workspace,
+                                        (hipStream_t)hip_stream);
+  return e == hipSuccess ? DSV_OK : DSV_ERR_HIP;
+}
+
 int dsv_dvl_allocate_pack(const float *pred_logits, const int32_t *num_live,
                           const int32_t *tokens, const int32_t *positions,
                           const int32_t *kv_refs, int32_t *k_out,

@@ -83,6 +83,16 @@ hipError_t launch_accept_stochastic(const void *logits, int dtype, const int32_t
                                     int32_t num_chunks, hipStream_t s);
 
 // -------------------------------------------------------------------------
+// acceptance predictor
+// -------------------------------------------------------------------------
+constexpr int kPredHidden = DSV_PRED_HIDDEN;
+size_t predictor_workspace_bytes(int32_t n_bs, int32_t in_dim);
+hipError_t launch_predictor(const float *features, const int32_t *num_live, const float *w1,
+                            const float *b1, const float *w2, const float *b2, float *out,
+                            int32_t n_bs, int32_t in_dim, int32_t out_dim, float *part,
+                            hipStream_t s);
+
+// -------------------------------------------------------------------------
 // DVL allocation and packing
 // -------------------------------------------------------------------------
 hipError_t launch_dvl(const float *pred_logits, const int32_t *num_live,
@@ -99,7 +109,8 @@ enum TimingKind {
   kTimePrefix = 3,
   kTimeDvl = 4,
   kTimeSampleStats = 5,
-  kTimeSampleDraw = 6
+  kTimeSampleDraw = 6,
+  kTimePredictor = 7
 };
 // Records a HIP event before (end = false) or after (end = true) a launch
 // when timing is on and the stream is not being captured.

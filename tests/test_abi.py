@@ -177,3 +177,21 @@ def test_accept_stochastic_rejects_bad_arguments():
     assert lib.dsv_accept_stochastic(*bad) == -3
     bad = list(args); bad[12] = need - 1
     assert lib.dsv_accept_stochastic(*bad) == -4
+
+
+def test_predictor_rejects_bad_arguments():
+    lib = dsv.load()
+    fake = 1 << 20
+    need = lib.dsv_predictor_workspace_bytes(32, 1735)
+    assert need == 28 * 32 * 64 * 4 and lib.dsv_predictor_workspace_bytes(0, 1735) == 0
+    args = [fake] * 7 + [32, 1735, 64, 15, fake, need, None]
+    bad = list(args); bad[2] = None
+    assert lib.dsv_predictor_forward(*bad) == -1
+    bad = list(args); bad[7] = dsv.DVL_MAX_REQS + 1
+    assert lib.dsv_predictor_forward(*bad) == -2
+    bad = list(args); bad[10] = 0
+    assert lib.dsv_predictor_forward(*bad) == -2
+    bad = list(args); bad[9] = 32
+    assert lib.dsv_predictor_forward(*bad) == -3
+    bad = list(args); bad[12] = need - 1
+    assert lib.dsv_predictor_forward(*bad) == -4
