@@ -187,12 +187,13 @@ def stress_bench(steps):
 
 
 def dvl_bench(launches=100, replays=10):
-    """DVL allocate-and-pack (Sec. III-C, Alg. 1) per launch: ``launches``
-    back-to-back calls captured in one hipGraph, replayed ``replays`` times
-    and timed with HIP events on the capturing stream, for the B=32 bucket of
-    the workload and two larger buckets.  Inputs: make_dvl_inputs (synthetic
-    predictor logits with per-request geometric profiles), all slots live.
-    The kernel is one workgroup, so it is bound by latency, not by HBM: the
+    """The decision step (Sec. III-C, Alg. 1, Eq. (5)) per launch: the
+    acceptance predictor (1735-64-15), DVL allocate-and-pack, and the two
+    back to back.  Each is ``launches`` calls captured in one hipGraph,
+    replayed ``replays`` times and timed with HIP events on the capturing
+    stream, for the B=32 bucket of the workload and two larger buckets.
+    Inputs: make_predictor_inputs / make_dvl_inputs, all slots live.  One
+    workgroup (DVL) or a few (predictor): bound by latency, not by HBM; the
     bytes are given for reference only."""
     import torch
 
@@ -202,34 +203,44 @@ def dvl_bench(launches=100, replays=10):
     out = {}
     for n_bs in (32, 256, 1024):
         w = W.BLOCK_WIDTH
-        d = W.make_dvl_inputs(np.random.default_rng(W.SEED_BASE + 60 + n_bs), n_bs=n_bs,
-                              n_live=n_bs)
+        rng = np.random.default_rng(W.SEED_BASE + 60 + n_bs)
+        d = W.make_dvl_inputs(rng, n_bs=n_bs, n_live=n_bs)
+        p = W.make_predictor_inputs(rng, n_bs=n_bs, n_live=n_bs)
         m_bs = w * n_bs // 2
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
         lg, tok, pos, ref = dev(d.pred_logits), dev(d.tokens), dev(d.positions), dev(d.kv_refs)
+        feats, w1, b1, w2, b2 = (dev(x) for x in (p.features, p.w1, p.b1, p.w2, p.b2))
+        ws_pred = dsv.alloc_workspace(dsv.predictor_workspace_bytes(n_bs, p.features.shape[1]),
+                                      "cuda")
         nl = dev(np.array([n_bs], np.int32))
         z = lambda n: torch.zeros(n, dtype=torch.int32, device="cuda")
         k, cu, pt, pp, pr = z(n_bs), z(n_bs + 1), z(m_bs), z(m_bs), z(m_bs)
         s = torch.cuda.Stream()
-        call = lambda: dsv.dvl_allocate_pack(lg, nl, tok, pos, ref, k, cu, pt, pp, pr, stream=s)
-        for _ in range(10):
-            call()
-        torch.cuda.synchronize()
-        g = dsv.Graph().capture(lambda: [call() for _ in range(launches)], s)
-        g.replay(s)
-        torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(s)
-        for _ in range(replays):
+        dvl = lambda: dsv.dvl_allocate_pack(lg, nl, tok, pos, ref, k, cu, pt, pp, pr, stream=s)
+        pred = lambda: dsv.predictor_forward(feats, nl, w1, b1, w2, b2, lg, workspace=ws_pred,
+                                             stream=s)
+        both = lambda: (pred(), dvl())
+        res = {}
+        for name, fn in (("dvl", dvl), ("predictor", pred), ("predictor_then_dvl", both)):
+            for _ in range(10):
+                fn()
+            torch.cuda.synchronize()
+            g = dsv.Graph().capture(lambda: [fn() for _ in range(launches)], s)
             g.replay(s)
-        e1.record(s)
-        torch.cuda.synchronize()
-        g.close()
-        us = e0.elapsed_time(e1) * 1e3 / (launches * replays)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            for _ in range(replays):
+                g.replay(s)
+            e1.record(s)
+            torch.cuda.synchronize()
+            g.close()
+            res[name + "_us"] = round(e0.elapsed_time(e1) * 1e3 / (launches * replays), 2)
         nbytes = n_bs * (w - 1) * 4 + 3 * m_bs * 4 + 8 + (2 * n_bs + 1) * 4 + 3 * m_bs * 4
-        out["n_bs_%d" % n_bs] = {"us_per_call": round(us, 2), "algorithmic_bytes": nbytes}
-    out["bound"] = "latency (one workgroup)"
+        res["dvl_algorithmic_bytes"] = nbytes
+        out["n_bs_%d" % n_bs] = res
+    out["bound"] = "latency (one workgroup for DVL; K-split tiles for the predictor)"
     out["timing"] = "%d launches in one hipGraph, %d replays, HIP events" % (launches, replays)
     return out
 
@@ -237,7 +248,8 @@ def dvl_bench(launches=100, replays=10):
 def bucket_bench(layers=4, reps=5):
     """The multi-bucket capture set (Sec. III-D, Alg. 2, Eqs. (13)-(15)):
     buckets {8, 16, 32, 64} sharing one attention and one acceptance
-    workspace, each with a captured decision graph (DVL) and verify graph
+    workspace, each with a captured decision graph (predictor + DVL) and
+    verify graph
     (``layers`` attention layers, Qwen3-8B shape, then acceptance over
     151,936 tokens).  Per bucket, at N = N_bs and at N = 3 N_bs / 4 (the rest
     sentinels): decision and verify replay times (HIP events on the replay
@@ -262,8 +274,11 @@ def bucket_bench(layers=4, reps=5):
     gen.manual_seed(W.SEED_BASE + 81)
     kv = [torch.randn((num_pages, 2, hkv, W.PAGE_SIZE * d), generator=gen, device="cuda",
                       dtype=torch.bfloat16) for _ in range(layers)]
+    p0 = W.make_predictor_inputs(rng, n_bs=pool, n_live=pool)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+    pred = dict(w1=t(p0.w1), b1=t(p0.b1), w2=t(p0.w2), b2=t(p0.b2))
     bs = dsv.BucketSet(sizes, kv_pools=kv, max_pages=max_pages, max_kv_len=max_kv_len,
-                       num_q_heads=hq, head_dim=d, vocab=V)
+                       num_q_heads=hq, head_dim=d, vocab=V, predictor=pred)
     s = torch.cuda.Stream()
     bs.capture(s)
     rows = []
@@ -276,7 +291,8 @@ def bucket_bench(layers=4, reps=5):
             for _ in range(reps):
                 reqs = np.sort(rng.choice(pool, size=n, replace=False))
                 dv = W.make_dvl_inputs(rng, n_bs=b, n_live=n)
-                bk.stage_decision(n, dv.pred_logits, dv.tokens, dv.positions, dv.kv_refs)
+                feats = W.make_predictor_inputs(rng, n_bs=b, n_live=n).features
+                bk.stage_decision(n, feats, dv.tokens, dv.positions, dv.kv_refs)
                 bk.stage_verify(n, ctx_all[reqs], cache_map[reqs])
                 torch.cuda.synchronize()
                 ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]

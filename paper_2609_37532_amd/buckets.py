@@ -5,7 +5,8 @@ For every bucket size N_bs the set allocates, once, every buffer the decision
 step and the verify step touch (so their addresses and shapes never change,
 Eq. (13)), and captures two graphs:
 
-* the decision graph: DVL allocation and packing (``dvl_allocate_pack``),
+* the decision graph: the acceptance predictor (``predictor_forward``, when
+  weights are given) and DVL allocation and packing (``dvl_allocate_pack``),
   which writes the lengths, offsets and packed rows into the bucket's buffers;
 * the verify graph: verify attention for every layer, then greedy
   acceptance, reading the offsets and packed tokens the decision graph wrote.
@@ -38,7 +39,7 @@ class Bucket:
 
     def __init__(self, n_bs: int, *, kv_pools: Sequence, max_pages: int, max_kv_len: int,
                  num_q_heads: int, head_dim: int, vocab: int, width: int, device,
-                 ws_attn=None, ws_acc=None):
+                 ws_attn=None, ws_acc=None, predictor: Optional[dict] = None, ws_pred=None):
         import torch
 
         self.torch = torch
@@ -51,6 +52,17 @@ class Bucket:
         z = lambda *shape, dtype=i32: torch.zeros(shape, dtype=dtype, device=device)
         # decision step: inputs staged each step, outputs written by the graph
         self.pred_logits = z(n_bs, w - 1, dtype=f32)
+        self.predictor = predictor
+        self.features = None
+        if predictor is not None:
+            in_dim = predictor["w1"].shape[0]
+            if predictor["w2"].shape[1] != w - 1:
+                raise ValueError("the predictor must output W-1 logits")
+            self.features = z(n_bs, in_dim, dtype=f32)
+            need = _lib.predictor_workspace_bytes(n_bs, in_dim)
+            if ws_pred is not None and ws_pred.numel() < need:
+                raise ValueError("shared workspace too small")
+            self.ws_pred = ws_pred if ws_pred is not None else _lib.alloc_workspace(need, device)
         self.num_live = z(1)
         self.tokens, self.positions, self.kv_refs = z(n_bs, w), z(n_bs, w), z(n_bs, w)
         self.k, self.cu = z(n_bs), z(n_bs + 1)
@@ -80,6 +92,11 @@ class Bucket:
 
     # -------------------------------------------------------------- enqueue
     def enqueue_decision(self, stream) -> None:
+        if self.predictor is not None:
+            p = self.predictor
+            _lib.predictor_forward(self.features, self.num_live, p["w1"], p["b1"], p["w2"],
+                                   p["b2"], self.pred_logits, workspace=self.ws_pred,
+                                   stream=stream)
         _lib.dvl_allocate_pack(self.pred_logits, self.num_live, self.tokens, self.positions,
                                self.kv_refs, self.k, self.cu, self.packed_tokens,
                                self.packed_positions, self.packed_kv_refs, stream=stream)
@@ -115,14 +132,17 @@ class Bucket:
     def stage_decision(self, n_live: int, pred_logits, tokens, positions, kv_refs) -> None:
         """Copy one step's decision inputs for the first ``n_live`` slots
         (host arrays or device tensors of n_live rows); the sentinel rows
-        keep whatever they held (they are not used).  The copies go on
+        keep whatever they held (they are not used).  With a predictor,
+        ``pred_logits`` is the feature matrix [n_live, in_dim] instead (the
+        predictor computes the logits inside the graph).  The copies go on
         torch's current stream; the caller has synchronised the previous
         step's replays (Alg. 2 reads its outputs first)."""
         torch = self.torch
         if not 0 <= n_live <= self.n_bs:
             raise ValueError("live count %d outside bucket %d" % (n_live, self.n_bs))
         self.num_live.fill_(n_live)
-        for dst, src in ((self.pred_logits, pred_logits), (self.tokens, tokens),
+        first = self.features if self.predictor is not None else self.pred_logits
+        for dst, src in ((first, pred_logits), (self.tokens, tokens),
                          (self.positions, positions), (self.kv_refs, kv_refs)):
             if n_live:
                 dst[:n_live].copy_(torch.as_tensor(src)[:n_live], non_blocking=False)
@@ -162,7 +182,9 @@ class Bucket:
         workspaces, the activation stand-ins (q, out, logits) and the two
         graph instantiations."""
         nb = lambda *ts: int(sum(t.numel() * t.element_size() for t in ts))
+        extra = (self.features,) if self.features is not None else ()
         meta = nb(self.pred_logits, self.num_live, self.tokens, self.positions, self.kv_refs,
+                  *extra,
                   self.k, self.cu, self.packed_tokens, self.packed_positions,
                   self.packed_kv_refs, self.ctx_lens, self.page_table, self.accept_len,
                   self.next_token)
@@ -179,7 +201,10 @@ class BucketSet:
 
     def __init__(self, buckets: Iterable[int], *, kv_pools: Sequence, max_pages: int,
                  max_kv_len: int, num_q_heads: int, head_dim: int, vocab: int,
-                 width: int = _lib.MAX_QLEN, device=None):
+                 width: int = _lib.MAX_QLEN, device=None, predictor: Optional[dict] = None):
+        """``predictor``: optional dict of device tensors w1 [in, 64], b1 [64],
+        w2 [64, W-1], b2 [W-1]; with it each decision graph runs the predictor
+        on staged features before DVL (Alg. 2's Features -> DVL pipeline)."""
         import torch
 
         sizes = sorted(set(int(b) for b in buckets))
@@ -201,10 +226,15 @@ class BucketSet:
         need_acc = max(_lib.accept_workspace_bytes(width * b // 2, b, vocab) for b in sizes)
         self.ws_attn = _lib.alloc_workspace(need_attn, dev)
         self.ws_acc = _lib.alloc_workspace(need_acc, dev)
+        self.ws_pred = None
+        if predictor is not None:
+            self.ws_pred = _lib.alloc_workspace(
+                _lib.predictor_workspace_bytes(big, predictor["w1"].shape[0]), dev)
         self.buckets: Dict[int, Bucket] = {
             b: Bucket(b, kv_pools=kv_pools, max_pages=max_pages, max_kv_len=max_kv_len,
                       num_q_heads=num_q_heads, head_dim=head_dim, vocab=vocab, width=width,
-                      device=dev, ws_attn=self.ws_attn, ws_acc=self.ws_acc)
+                      device=dev, ws_attn=self.ws_attn, ws_acc=self.ws_acc,
+                      predictor=predictor, ws_pred=self.ws_pred)
             for b in sizes}
 
     def select(self, n: int) -> int:
@@ -225,7 +255,8 @@ class BucketSet:
         """Per-bucket figures (their workspace entry is the shared pair) and
         the set's totals."""
         per = [self.buckets[b].memory() for b in self.sizes]
-        ws = int(self.ws_attn.numel() + self.ws_acc.numel())
+        ws = int(self.ws_attn.numel() + self.ws_acc.numel()
+                 + (self.ws_pred.numel() if self.ws_pred is not None else 0))
         keys = ("metadata_bytes", "activation_bytes", "graph_decision_bytes",
                 "graph_verify_bytes")
         total = {k: int(sum(m[k] for m in per)) for k in keys}

@@ -40,16 +40,25 @@ __global__ __launch_bounds__(kThreads) void mlp_hidden_partial_kernel(
   if (r0 >= n) return;  // no live row in this tile: its partials are never read
   const int k0 = ks * kKT;
   // W1 slice (rows of 64 contiguous weights) and the feature tile, zero past
-  // the last feature and the live rows
-  for (int idx = tid; idx < kKT * kH; idx += kThreads) {
-    const int kk = idx / kH, u = idx % kH;
-    const int k = k0 + kk;
-    sw[kk][u] = k < in_dim ? w1[(size_t)k * kH + u] : 0.f;
+  // the last feature and the live rows: every load is issued before the
+  // first LDS store (clamped addresses instead of branches)
+  constexpr int kPer = kKT * kH / kThreads;  // 16 of each per thread
+  float wv[kPer], fv[kPer];
+#pragma unroll
+  for (int it = 0; it < kPer; ++it) {
+    const int idx = tid + it * kThreads;
+    const int k = k0 + idx / kH;
+    wv[it] = w1[(size_t)(k < in_dim ? k : in_dim - 1) * kH + idx % kH];
+    const int row = r0 + idx / kKT, kf = k0 + idx % kKT;
+    const bool ok = row < n && kf < in_dim;
+    fv[it] = features[ok ? (size_t)row * in_dim + kf : 0];
   }
-  for (int idx = tid; idx < kRT * kKT; idx += kThreads) {
-    const int r = idx / kKT, kk = idx % kKT;
-    const int row = r0 + r, k = k0 + kk;
-    sf[r][kk] = (row < n && k < in_dim) ? features[(size_t)row * in_dim + k] : 0.f;
+#pragma unroll
+  for (int it = 0; it < kPer; ++it) {
+    const int idx = tid + it * kThreads;
+    sw[idx / kH][idx % kH] = k0 + idx / kH < in_dim ? wv[it] : 0.f;
+    const int row = r0 + idx / kKT, kf = k0 + idx % kKT;
+    sf[idx / kKT][idx % kKT] = (row < n && kf < in_dim) ? fv[it] : 0.f;
   }
   __syncthreads();
   // thread: hidden unit h for 16 requests; features are LDS broadcasts
@@ -83,15 +92,27 @@ __global__ __launch_bounds__(kWave) void mlp_output_kernel(
     for (int j = lane; j < out_dim; j += kWave) out[(size_t)i * out_dim + j] = 0.f;
     return;
   }
+  // slice partials in slice order, eight loads in flight at a time
   float hsum = 0.f;
-  for (int s = 0; s < n_slices; ++s) hsum += part[((size_t)s * n_bs + i) * kH + lane];
+  int s = 0;
+  for (; s + 8 <= n_slices; s += 8) {
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = part[((size_t)(s + q) * n_bs + i) * kH + lane];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) hsum += v[q];
+  }
+  for (; s < n_slices; ++s) hsum += part[((size_t)s * n_bs + i) * kH + lane];
   hsum += b1[lane];
   sh[lane] = hsum > 0.f ? hsum : 0.f;
   __syncthreads();
   for (int j = lane; j < out_dim; j += kWave) {
+    float wc[kH];
+#pragma unroll
+    for (int u = 0; u < kH; ++u) wc[u] = w2[(size_t)u * out_dim + j];
     float o = 0.f;
-#pragma unroll 8
-    for (int u = 0; u < kH; ++u) o += sh[u] * w2[(size_t)u * out_dim + j];
+#pragma unroll
+    for (int u = 0; u < kH; ++u) o += sh[u] * wc[u];
     out[(size_t)i * out_dim + j] = o + b2[j];
   }
 }

@@ -112,3 +112,39 @@ def test_bucket_set_decision_then_verify():
             say("buckets", "step", step, "ok")
     finally:
         bs.close()
+
+
+def test_bucket_decision_graph_with_predictor():
+    # Alg. 2's decision pipeline: features -> predictor -> DVL in one graph
+    rng = np.random.default_rng(W.SEED_BASE + 72)
+    pool_reqs, max_kv_len = 16, 512 + W.BLOCK_WIDTH
+    max_pages = -(-max_kv_len // W.PAGE_SIZE)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(W.SEED_BASE + 73)
+    kv_pools = [torch.randn((pool_reqs * max_pages, 2, HKV, W.PAGE_SIZE * D), generator=gen,
+                            device=DEV, dtype=torch.bfloat16)]
+    p0 = W.make_predictor_inputs(rng, n_bs=16, n_live=16)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    pred = dict(w1=t(p0.w1), b1=t(p0.b1), w2=t(p0.w2), b2=t(p0.b2))
+    bs = dsv.BucketSet((8, 16), kv_pools=kv_pools, max_pages=max_pages, max_kv_len=max_kv_len,
+                       num_q_heads=HQ, head_dim=D, vocab=V, predictor=pred)
+    s = torch.cuda.Stream(device=DEV)
+    bs.capture(s)
+    try:
+        for step, n in enumerate((16, 9, 8, 3)):
+            bk = bs[bs.select(n)]
+            feats = W.make_predictor_inputs(rng, n_bs=bk.n_bs, n_live=n).features
+            d = W.make_dvl_inputs(rng, n_bs=bk.n_bs, n_live=n, vocab=V)
+            bk.stage_decision(n, feats, d.tokens, d.positions, d.kv_refs)
+            bk.replay_decision(s)
+            s.synchronize()
+            logits = bk.pred_logits.cpu().numpy()
+            want = oracle.predictor_forward(feats, n, p0.w1, p0.b1, p0.w2, p0.b2)
+            assert np.allclose(logits[:n], want[:n], rtol=1e-4, atol=1e-4)
+            ref = oracle.dvl_allocate_pack(logits, n, d.tokens, d.positions, d.kv_refs)
+            assert np.array_equal(bk.k.cpu().numpy(), ref["k"])
+            assert np.array_equal(bk.cu.cpu().numpy(), ref["offsets"])
+            assert np.array_equal(bk.packed_tokens.cpu().numpy(), ref["tokens"])
+            say("buckets", "predictor step", step, "live", n, "bucket", bk.n_bs, "ok")
+    finally:
+        bs.close()
