@@ -186,6 +186,51 @@ def stress_bench(steps):
             "acceptance_exact_every_step": exact}
 
 
+def configs_bench(reps=50):
+    """Verify attention alone on the other attention presets (configs 2 and
+    3: Qwen3-4B shape B=8 with full blocks over contexts U[256, 2048], and
+    Qwen3-8B shape B=16 packed over U[512, 4096]) and config 4 for
+    reference: per launch, HIP events around each kernel on its stream."""
+    import torch
+
+    import paper_2609_37532_amd as dsv
+    import workloads as W
+
+    out = {}
+    for idx in (2, 3, 4):
+        attn = W.config_attn_inputs(idx)
+        bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to("cuda").view(
+            torch.bfloat16)
+        i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to("cuda")
+        q, kv = bf(attn.q), bf(attn.kv_pages)
+        cu, pt, ctx = i32(attn.cu_qlens), i32(attn.page_table), i32(attn.ctx_lens)
+        o = torch.zeros_like(q)
+        dims = dsv.attn_dims(q, kv, pt, max_kv_len=attn.max_kv_len, scale=attn.scale)
+        ws = dsv.alloc_workspace(dsv.verify_attn_workspace_bytes(dims), "cuda")
+        s = torch.cuda.Stream()
+        run = lambda: dsv.verify_attn(q, cu, kv, pt, ctx, o, dims=dims, workspace=ws, stream=s)
+        for _ in range(5):
+            run()
+        torch.cuda.synchronize()
+        with dsv.KernelTimer(max_launches=2 * reps + 8) as tm:
+            for _ in range(reps):
+                run()
+            torch.cuda.synchronize()
+        t_split = tm.mean_ms("attn_split") * 1e-3
+        t_comb = tm.mean_ms("attn_combine") * 1e-3
+        nbytes = attention_bytes(attn, attn.num_kv_heads, attn.num_q_heads, attn.head_dim)
+        toks = int(attn.qlens.sum())
+        out["config_%d" % idx] = {
+            "B": attn.num_reqs, "packed_tokens": toks, "algorithmic_bytes": nbytes,
+            "attn_us": round(t_split * 1e6, 2), "combine_us": round(t_comb * 1e6, 2),
+            "attn_gbps": round(nbytes / t_split / 1e9, 1),
+            "attn_frac": round(nbytes / t_split / 1e9 / HBM_PEAK_GBPS, 4),
+            "packed_tokens_per_s_attention": round(toks / (t_split + t_comb), 1)}
+        del q, kv, o
+        torch.cuda.empty_cache()
+    return out
+
+
 def dvl_bench(launches=100, replays=10):
     """The decision step (Sec. III-C, Alg. 1, Eq. (5)) per launch: the
     acceptance predictor (1735-64-15), DVL allocate-and-pack, and the two
@@ -490,6 +535,8 @@ def main():
     }
     graph.close()
 
+    log("configs 2-4 attention ...")
+    result["attention_configs"] = configs_bench()
     if args.no_next:
         finish(args, result, attn, acc, torch)
         return

@@ -141,10 +141,24 @@ __global__ __launch_bounds__(kWave) void prefix_kernel(
   if (k < 0 || k > kMaxQlen || o < 0 || o + k > cap) return;  // bad metadata
   int t = -1;
   if (lane < k) {
+    // the row's chunk pairs in chunk order, loaded kBatch at a time so that
+    // the loads of a batch are in flight together
+    constexpr int kBatch = 16;
     const size_t base = (size_t)(o + lane) * num_chunks;
-    float bv = best_val[base];
-    int bi = best_idx[base];
-    for (int c = 1; c < num_chunks; ++c) take(bv, bi, best_val[base + c], best_idx[base + c]);
+    float bv = -INFINITY;
+    int bi = 0x7FFFFFFF;
+    for (int c0 = 0; c0 < num_chunks; c0 += kBatch) {
+      float v[kBatch];
+      int x[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int c = min(c0 + u, num_chunks - 1);  // clamped: repeats are harmless
+        v[u] = best_val[base + c];
+        x[u] = best_idx[base + c];
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) take(bv, bi, v[u], x[u]);
+    }
     t = bi;
   }
   const bool mismatch = lane < k - 1 && t != draft[o + lane + 1];

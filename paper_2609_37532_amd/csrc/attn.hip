@@ -49,6 +49,11 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kBlockKeys = 32;  // keys per inner step (two pages)
+// Smallest stream-K share: with little work (short contexts, few requests)
+// eight blocks per workgroup beat spreading it over every resident
+// workgroup -- fewer cut segments, so less partial traffic and combine work,
+// and a longer pipeline per workgroup.
+constexpr int kMinShare = 8 * kBlockKeys;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8, v);
@@ -380,7 +385,7 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
   const int excl = before + incl - sum;  // prefix of this thread's first request
   const int work = total * p.hkv;
   int share = (work + (int)gridDim.x - 1) / (int)gridDim.x;
-  share = max(kBlockKeys, round_up_block(share));
+  share = max(kMinShare, round_up_block(share));
   const int start = (int)blockIdx.x * share;
   const int end = min(work, start + share);
   if (blockIdx.x == 0) {
