@@ -65,22 +65,27 @@ __device__ __forceinline__ float wave_incl_scan_f(float v) {
   return v;
 }
 
+// 2^x with the hardware instruction alone, without the library's denormal
+// range handling (a term below 2^-126 of the row maximum contributes
+// nothing); every kernel here uses it, so they agree on each term.
+__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // Online (max, sum of exp2(y - max)) accumulation of one scaled value.
 __device__ __forceinline__ void acc(float &m, float &s, float y) {
   if (y > m) {
-    s = s * exp2f(m - y) + 1.f;
+    s = s * fexp2(m - y) + 1.f;
     m = y;
   } else if (y > -INFINITY) {  // a -inf logit adds nothing
-    s += exp2f(y - m);
+    s += fexp2(y - m);
   }
 }
 
 __device__ __forceinline__ void merge(float &m, float &s, float om, float os) {
   if (om > m) {
-    s = s * exp2f(m - om) + os;
+    s = s * fexp2(m - om) + os;
     m = om;
   } else if (om != -INFINITY) {
-    s += os * exp2f(om - m);
+    s += os * fexp2(om - m);
   }
 }
 
@@ -148,7 +153,7 @@ __global__ __launch_bounds__(kThreads) void softmax_stats_kernel(
     float ls = 0.f;
     if (lm > -INFINITY) {
 #pragma unroll
-      for (int q = 0; q < kN; ++q) ls += exp2f(y[q] - lm);
+      for (int q = 0; q < kN; ++q) ls += fexp2(y[q] - lm);
     }
     merge(m, s, lm, ls);
   } else {
@@ -227,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
       float p = 0.f;
       if (x >= 0 && x < vocab) {
         const char *row = (const char *)logits + (size_t)(o + tid) * vocab * kEs;
-        p = exp2f(scaled(elem<kBf16>(row, x), c) - s_rm[tid]) / s_rz[tid];
+        p = fexp2(scaled(elem<kBf16>(row, x), c) - s_rm[tid]) / s_rz[tid];
       }
       reject = !(uniforms[2 * (size_t)(o + tid)] < p);
     }
@@ -244,7 +249,7 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
     const int x = draft[r + 1];
     removed = (x >= 0 && x < vocab) ? x : -1;
   }
-  const float ex = removed >= 0 ? exp2f(scaled(elem<kBf16>(row, removed), c) - M) : 0.f;
+  const float ex = removed >= 0 ? fexp2(scaled(elem<kBf16>(row, removed), c) - M) : 0.f;
 
   // The chunk holding the target mass: wave 0 takes 64 chunks at a time,
   // scans their masses in chunk order and picks the first chunk whose
@@ -262,7 +267,7 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
       float w = 0.f;
       if (ch < num_chunks) {
         const float sm = stat_m[base + ch];
-        w = sm == -INFINITY ? 0.f : stat_s[base + ch] * exp2f(sm - M);
+        w = sm == -INFINITY ? 0.f : stat_s[base + ch] * fexp2(sm - M);
         if (ch == rc) w = fmaxf(w - ex, 0.f);
       }
       const float incl = carry + wave_incl_scan_f(w);
@@ -314,7 +319,7 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
     for (int q = 0; q < kPerThread; ++q) {
       const int v = v0 + q;
       float ev = 0.f;
-      if (v < vocab && v != removed) ev = exp2f(scaled(elem<kBf16>(row, v), c) - M);
+      if (v < vocab && v != removed) ev = fexp2(scaled(elem<kBf16>(row, v), c) - M);
       e[q] = ev;
       mine += ev;
     }
