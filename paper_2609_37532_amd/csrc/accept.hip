@@ -139,11 +139,14 @@ __global__ __launch_bounds__(kWave) void prefix_kernel(
     return;
   }
   if (k < 0 || k > kMaxQlen || o < 0 || o + k > cap) return;  // bad metadata
+  // the drafted token each row is compared with, loaded with the chunk pairs
+  const int want = lane < k - 1 ? draft[o + lane + 1] : -1;
   int t = -1;
   if (lane < k) {
     // the row's chunk pairs in chunk order, loaded kBatch at a time so that
-    // the loads of a batch are in flight together
-    constexpr int kBatch = 16;
+    // the loads of a batch are in flight together (one batch up to 32
+    // chunks, a 262,144-token vocabulary)
+    constexpr int kBatch = 32;
     const size_t base = (size_t)(o + lane) * num_chunks;
     float bv = -INFINITY;
     int bi = 0x7FFFFFFF;
@@ -161,7 +164,7 @@ __global__ __launch_bounds__(kWave) void prefix_kernel(
     }
     t = bi;
   }
-  const bool mismatch = lane < k - 1 && t != draft[o + lane + 1];
+  const bool mismatch = lane < k - 1 && t != want;
   const unsigned long long mask = __ballot(mismatch);
   const int a = mask ? __builtin_ctzll(mask) : k - 1;
   const int succ = __shfl(t, a, kWave);

@@ -355,6 +355,7 @@ __device__ __forceinline__ void write_tile(const AttnParams &p, int g, bool comp
 struct Share {
   int start, end;
   int i, g, off;  // segment and key offset where `start` falls
+  ReqMeta first;  // request i's metadata, as read by the plan
 };
 
 // Computes the share with one block-wide scan over the requests' segment
@@ -366,8 +367,20 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
   const int per = (B + kThreads - 1) / kThreads;
   const int lo = min(B, tid * per), hi = min(B, lo + per);
   int sum = 0;
+  // with one request per thread (B <= 256) its metadata stays in registers
+  // for the locate step below
+  int q0 = 0, q1 = 0, cx = 0;
+  if (per == 1) {
+    if (lo < hi) {
+      q0 = p.cu[lo];
+      q1 = p.cu[lo + 1];
+      cx = p.ctx[lo];
+      sum = segment_of(p, q0, q1, cx);
+    }
+  } else {
 #pragma unroll 4
-  for (int i = lo; i < hi; ++i) sum += segment_len(p, i);
+    for (int i = lo; i < hi; ++i) sum += segment_len(p, i);
+  }
   int incl = sum;
 #pragma unroll
   for (int d = 1; d < kWave; d <<= 1) {
@@ -399,16 +412,25 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
       p.plan[B + 1] = share;
     }
   }
-  // the thread whose requests contain `start` locates it
+  // the thread whose requests contain `start` locates it and publishes the
+  // request's metadata, so the first piece needs no second read of it
   if (start < work && excl * p.hkv <= start && start < (excl + sum) * p.hkv) {
     int acc = excl;
     for (int i = lo; i < hi; ++i) {
-      const int seg = segment_len(p, i);
+      if (per != 1) {
+        q0 = p.cu[i];
+        q1 = p.cu[i + 1];
+        cx = p.ctx[i];
+      }
+      const int seg = segment_of(p, q0, q1, cx);
       if (start < (acc + seg) * p.hkv) {
         const int rel = start - acc * p.hkv;
         lds[kWaves + 0] = i;
         lds[kWaves + 1] = rel / seg;
         lds[kWaves + 2] = rel % seg;
+        lds[kWaves + 3] = q0;
+        lds[kWaves + 4] = q1;
+        lds[kWaves + 5] = cx;
         break;
       }
       acc += seg;
@@ -422,8 +444,16 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
     sh.i = __builtin_amdgcn_readfirstlane(lds[kWaves + 0]);
     sh.g = __builtin_amdgcn_readfirstlane(lds[kWaves + 1]);
     sh.off = __builtin_amdgcn_readfirstlane(lds[kWaves + 2]);
+    const int f0 = __builtin_amdgcn_readfirstlane(lds[kWaves + 3]);
+    const int f1 = __builtin_amdgcn_readfirstlane(lds[kWaves + 4]);
+    sh.first.q0 = f0;
+    sh.first.ctx = __builtin_amdgcn_readfirstlane(lds[kWaves + 5]);
+    sh.first.k = f1 - f0;
+    sh.first.len = sh.first.ctx + sh.first.k;
+    sh.first.seg = segment_of(p, f0, f1, sh.first.ctx);
   } else {
     sh.i = sh.g = sh.off = 0;
+    sh.first = ReqMeta{0, 0, 0, 0, 0};
   }
   return sh;
 }
@@ -509,7 +539,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
   using R = Ring<D>;
   __shared__ __attribute__((aligned(1024))) char ring[kStages * R::kStage];
   __shared__ int pg[kSubPages + 8];
-  __shared__ int lds_plan[kWaves + 4];
+  __shared__ int lds_plan[kWaves + 6];
 
   const Share sh = plan_share(p, lds_plan);
   if (sh.start >= sh.end) return;
@@ -530,7 +560,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
 
   int i = sh.i, g = sh.g, off = sh.off, pos = sh.start, piece = 0;
   while (pos < sh.end && i < p.num_reqs) {
-    const ReqMeta rq = load_req(p, i);
+    const ReqMeta rq = piece == 0 && i == sh.i ? sh.first : load_req(p, i);
     if (rq.seg == 0) {  // sentinel or bad metadata: no keys in the plan
       ++i;
       continue;
@@ -645,6 +675,8 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
     }
     return;
   }
+  // the request's metadata is read together with the plan (one round trip)
+  const ReqMeta rq = load_req(p, i);
   const int prefix = p.plan[i];
   const int seg = p.plan[i + 1] - prefix;  // p.plan[B] is the total
   if (seg <= 0) return;
@@ -652,7 +684,6 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
   const int start = prefix * p.hkv + g * seg;
   const int b0 = start / share, b1 = (start + seg - 1) / share;
   if (b0 == b1) return;  // one workgroup held the whole segment
-  const ReqMeta rq = load_req(p, i);
   const int rr = blockIdx.x * kRows + threadIdx.x / kLanesPerRow;
   if (rr >= G * rq.k) return;
   const int d4 = threadIdx.x % kLanesPerRow;
