@@ -81,6 +81,17 @@ def test_head_layouts(hq, hkv, d):
           "heads-%d-%d-d%d" % (hq, hkv, d))
 
 
+@pytest.mark.parametrize("B", [257, 700])
+def test_many_requests(B):
+    # more requests than plan threads: each plan thread owns several requests
+    # (and locates a share start among them); about one in six is a sentinel
+    rng = np.random.default_rng(B)
+    ctx = rng.integers(0, 400, size=B)
+    k = rng.integers(1, 17, size=B)
+    k[rng.random(B) < 0.17] = 0
+    check(case(B + 11, ctx, k, hq=8, hkv=2, d=64, max_kv_len=416), "many-requests-%d" % B)
+
+
 def test_long_context():
     check(case(77, [16000, 9000, 31], [4, 16, 2], max_kv_len=16384), "long-context")
 
