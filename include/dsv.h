@@ -151,6 +151,8 @@ size_t dsv_verify_attn_workspace_bytes(const dsv_attn_dims *dims);
  *   out         bf16 [capacity][Hq][D], written (every row).
  *   workspace   >= dsv_verify_attn_workspace_bytes(dims) bytes, 256-byte
  *               aligned.
+ * q_packed, kv_pages and out must be 16-byte aligned (every base allocation
+ * is); DSV_ERR_UNSUPPORTED otherwise, with nothing enqueued.
  * Precision: q.k products, the softmax and all accumulation are fp32; the
  * softmax weights enter the weighted sum of V rounded to bf16 (and the same
  * rounded weights form the normaliser); `out` is rounded once to bf16

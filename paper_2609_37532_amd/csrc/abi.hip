@@ -80,6 +80,9 @@ int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
     return DSV_ERR_NULL;
   const int rc = check_dims(dims);
   if (rc != DSV_OK) return rc;
+  // q rows, K/V tiles and out rows move in 16-byte vectors
+  if (((uintptr_t)q_packed | (uintptr_t)kv_pages | (uintptr_t)out) & 15u)
+    return DSV_ERR_UNSUPPORTED;
   const AttnWorkspace ws = attn_workspace_layout(*dims);
   if (!workspace || !aligned256(workspace) || workspace_bytes < ws.total)
     return DSV_ERR_WORKSPACE;

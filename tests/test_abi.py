@@ -86,6 +86,11 @@ def test_verify_attn_null_and_workspace_errors():
                                None, need, None) == -4
     assert lib.dsv_verify_attn(fake, fake, fake, fake, fake, fake, ctypes.byref(d),
                                fake + 8, need, None) == -4
+    # q, kv and out move in 16-byte vectors: misaligned views are refused
+    for arg in (0, 2, 5):
+        ptrs = [fake] * 6
+        ptrs[arg] = fake + 2
+        assert lib.dsv_verify_attn(*ptrs, ctypes.byref(d), fake, need, None) == -3, arg
 
 
 def test_workspace_is_bounded_by_the_grid_not_the_context():
