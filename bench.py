@@ -84,6 +84,22 @@ def accept_bytes(acc, esize):
     return live * acc.vocab * esize + live * 4 + (acc.num_reqs + 1) * 4 + 2 * acc.num_reqs * 4
 
 
+def row_padding(qlens, group):
+    """Inactive-row fractions of the batch under Eq. (2): rows(l, B) =
+    B*ceil(l/B), padding = 1 - l/rows, summed over live requests.  The
+    paper's tiles hold one request's l = k_i rows of one head (B = 128 native,
+    B = 16 with tile routing); this kernel stacks the G heads that share a KV
+    head, so its 16-row MFMA tiles hold l = G*k_i rows."""
+    k = np.asarray(qlens, dtype=np.int64)
+    k = k[k > 0]
+
+    def pad(l, b):
+        return 1.0 - float(l.sum()) / float((b * -(-l // b)).sum())
+    return {"paper_128_row_tiles": round(pad(k, 128), 4),
+            "paper_16_row_tiles": round(pad(k, 16), 4),
+            "live_row_mfma_tiles": round(pad(group * k, 16), 4)}
+
+
 def attention_flops(attn, hq, d):
     """q.k and p.v flops over the visible keys of every live row."""
     tot = 0
@@ -549,6 +565,7 @@ def main():
             "kv_tokens": int((attn.ctx_lens + attn.qlens).sum()),
             "capacity": attn.capacity,
             "step": "one hipGraph replay: attn stream-K + combine + argmax + prefix",
+            "row_padding_eq2": row_padding(attn.qlens, hq // hkv),
         },
         "roofline": {
             "bound": "hbm",

@@ -50,3 +50,15 @@ def test_cpu_threads_is_bounded(monkeypatch):
     assert 1 <= bench.cpu_threads() <= 16
     monkeypatch.setenv("OMP_NUM_THREADS", "100000")
     assert bench.cpu_threads() <= (__import__("os").cpu_count() or 1)
+
+
+def test_row_padding_eq2_by_hand():
+    # k = 16, 5, 1 live (and a sentinel) at G = 4: the paper's tiles hold k
+    # rows per head, the live-row tiles hold 4k rows (64, 20, 4 -> 4, 2, 1
+    # tiles of 16)
+    p = bench.row_padding([16, 5, 0, 1], 4)
+    assert p["paper_128_row_tiles"] == round(1 - 22 / 384, 4)
+    assert p["paper_16_row_tiles"] == round(1 - 22 / 48, 4)
+    assert p["live_row_mfma_tiles"] == round(1 - 88 / 112, 4)
+    # a full block leaves no padding at tile height 16
+    assert bench.row_padding([16], 1)["paper_16_row_tiles"] == 0.0
