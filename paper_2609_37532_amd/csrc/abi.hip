@@ -114,7 +114,7 @@ int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
 }
 
 size_t dsv_accept_workspace_bytes(int32_t capacity, int32_t num_reqs, int32_t vocab) {
-  if (capacity < 1 || num_reqs < 1 || vocab < 1) return 0;
+  if (capacity < 1 || capacity > 65535 || num_reqs < 1 || vocab < 1) return 0;
   return accept_workspace_layout(capacity, vocab).total;
 }
 

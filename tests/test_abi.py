@@ -112,6 +112,9 @@ def test_accept_rejects_bad_arguments():
     need = lib.dsv_accept_workspace_bytes(256, 32, 151936)
     assert need > 0 and need % 256 == 0
     assert lib.dsv_accept_workspace_bytes(0, 32, 151936) == 0
+    assert lib.dsv_accept_workspace_bytes(65536, 32, 151936) == 0
+    # the counters sit at fixed offsets: a larger size never needs less space
+    assert lib.dsv_accept_workspace_bytes(64, 8, 151936) <= need
     args = [fake, 1, fake, fake, fake, fake, 32, 256, 151936, fake, need, None]
     bad = list(args); bad[0] = None
     assert lib.dsv_accept(*bad) == -1

@@ -99,3 +99,46 @@ def test_many_requests_random_drafts():
     acc = W.make_accept_inputs(rng, cu_qlens=cu, capacity=int(cu[-1]) + 9, vocab=32000,
                                dtype="bf16", p_accept=0.2)
     check(acc, "64-requests")
+
+
+def test_all_sentinels():
+    # no live row at all: every request still gets the sentinel outputs
+    cu = np.zeros(4, np.int32)
+    lg = np.zeros((6, 500), np.float32)
+    acc = W.AcceptInputs(logits=lg, dtype="f32", cu_qlens=cu, draft_tokens=np.zeros(6, np.int32),
+                         planted_accept_len=np.zeros(3, np.int32),
+                         planted_next=np.full(3, -1, np.int32))
+    a, nxt = check(acc, "all-sentinels")
+    assert list(a) == [0, 0, 0] and list(nxt) == [-1, -1, -1]
+
+
+def test_one_workspace_across_calls():
+    # one workspace serves calls of two capacities in turn: eight calls in a
+    # row, with live rows changing (none at all in one of them) and new
+    # logits each time, are each exact
+    import torch
+    from gpu_util import DEV, bf16_dev, i32_dev
+    import paper_2609_37532_amd as dsv
+    B, cap, V = 12, 200, 30011
+    ws = dsv.alloc_workspace(dsv.accept_workspace_bytes(cap, B, V), DEV)
+    small_cap = 40  # every other call: a smaller capacity on the same workspace
+    a_dev = torch.zeros(B, dtype=torch.int32, device=DEV)
+    n_dev = torch.zeros(B, dtype=torch.int32, device=DEV)
+    rng = np.random.default_rng(123)
+    for call in range(8):
+        c = cap if call % 2 == 0 else small_cap
+        k = rng.integers(0, 17, size=B).astype(np.int32)
+        while int(k.sum()) > c:
+            k[int(np.argmax(k))] -= 1
+        if call == 3:
+            k[:] = 0
+        cu = W.cu_from_lengths(k)
+        acc = W.make_accept_inputs(rng, cu_qlens=cu, capacity=c, vocab=V, dtype="bf16",
+                                   p_accept=0.35)
+        say("accept", "workspace reuse", "call %d live rows %d" % (call, int(cu[-1])))
+        dsv.accept(bf16_dev(acc.logits), i32_dev(cu), i32_dev(acc.draft_tokens), a_dev, n_dev,
+                   workspace=ws)
+        torch.cuda.synchronize()
+        ra, rn = oracle.accept(acc.logits, acc.dtype, acc.cu_qlens, acc.draft_tokens)
+        assert np.array_equal(a_dev.cpu().numpy(), ra), call
+        assert np.array_equal(n_dev.cpu().numpy(), rn), call
