@@ -180,7 +180,15 @@ __global__ __launch_bounds__(kThreads) void softmax_stats_kernel(
   }
 }
 
+// Chunk statistics kept in LDS for the chunk scan of the drawn row (up to
+// this many chunks per row, a 524,288-token vocabulary; beyond it they are
+// read again from global memory).
+constexpr int kStashChunks = 64;
+
 // One workgroup per request: accept decisions, then the successor draw.
+// Everything that does not depend on another load is issued first: the
+// chunk statistics of the k rows, the drafted ids with both uniforms of
+// each row, and then the logit at each drafted id.
 template <bool kBf16>
 __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
     const void *logits, const int32_t *cu, const int32_t *draft, const float *uniforms,
@@ -188,7 +196,9 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
     int32_t num_chunks, float c, const float *stat_m, const float *stat_s) {
   constexpr int kEs = kBf16 ? 2 : 4;
   __shared__ float s_rm[kMaxQlen], s_rz[kMaxQlen];
-  __shared__ int s_a;
+  __shared__ float s_sm[kMaxQlen][kStashChunks], s_ss[kMaxQlen][kStashChunks];
+  __shared__ int s_a, s_removed;
+  __shared__ float s_ex, s_u1;
   __shared__ int s_chunk;
   __shared__ float s_target;  // mass still to cover inside the chosen chunk
   __shared__ float s_part[kThreads];  // inclusive token-order sums per thread
@@ -202,6 +212,21 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
     return;
   }
   if (k < 0 || k > kMaxQlen || o < 0 || o + k > cap) return;  // bad metadata
+  const bool stash = num_chunks <= kStashChunks;
+
+  // wave 0, lane j < k: the drafted id tested at row o+j, both uniforms of
+  // the row, and the logit at that id
+  int x = -1;
+  float u0 = 0.f, u1 = 0.f, lx = 0.f;
+  if (tid < k) {
+    u0 = uniforms[2 * (size_t)(o + tid)];
+    u1 = uniforms[2 * (size_t)(o + tid) + 1];
+    if (tid < k - 1) {
+      const int d = draft[o + tid + 1];
+      x = (d >= 0 && d < vocab) ? d : -1;
+    }
+  }
+  if (x >= 0) lx = elem<kBf16>((const char *)logits + (size_t)(o + tid) * vocab * kEs, x);
 
   // row normalisers: 16 lanes per row merge that row's chunk pairs in order
   {
@@ -209,7 +234,14 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
     float m = -INFINITY, s = 0.f;
     if (j < k) {
       const size_t base = (size_t)(o + j) * num_chunks;
-      for (int ch = l; ch < num_chunks; ch += 16) merge(m, s, stat_m[base + ch], stat_s[base + ch]);
+      for (int ch = l; ch < num_chunks; ch += 16) {
+        const float cm = stat_m[base + ch], cs = stat_s[base + ch];
+        if (stash) {
+          s_sm[j][ch] = cm;
+          s_ss[j][ch] = cs;
+        }
+        merge(m, s, cm, cs);
+      }
     }
 #pragma unroll
     for (int d = 8; d >= 1; d >>= 1) {
@@ -224,32 +256,32 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
   }
   __syncthreads();
 
-  // accept decisions: wave 0, lane j tests candidate j
+  // accept decisions: wave 0, lane j tests candidate j (accepted iff its
+  // uniform lies below P(x)); lane a also holds the drawn row's removed
+  // token, its unnormalised mass and the draw uniform
   if (tid < kWave) {
     bool reject = false;
+    float num = 0.f;
     if (tid < k - 1) {
-      const int x = draft[o + tid + 1];
-      float p = 0.f;
-      if (x >= 0 && x < vocab) {
-        const char *row = (const char *)logits + (size_t)(o + tid) * vocab * kEs;
-        p = fexp2(scaled(elem<kBf16>(row, x), c) - s_rm[tid]) / s_rz[tid];
-      }
-      reject = !(uniforms[2 * (size_t)(o + tid)] < p);
+      if (x >= 0) num = fexp2(scaled(lx, c) - s_rm[tid]);
+      reject = !(u0 < num / s_rz[tid]);
     }
     const unsigned long long mask = __ballot(reject);
-    if (tid == 0) s_a = mask ? __builtin_ctzll(mask) : k - 1;
+    const int a = mask ? __builtin_ctzll(mask) : k - 1;
+    if (tid == a) {
+      s_a = a;
+      s_removed = a < k - 1 ? x : -1;
+      s_ex = a < k - 1 ? num : 0.f;
+      s_u1 = u1;
+    }
   }
   __syncthreads();
   const int a = s_a;
   const int r = o + a;
   const char *row = (const char *)logits + (size_t)r * vocab * kEs;
   const float M = s_rm[a];
-  int removed = -1;
-  if (a < k - 1) {
-    const int x = draft[r + 1];
-    removed = (x >= 0 && x < vocab) ? x : -1;
-  }
-  const float ex = removed >= 0 ? fexp2(scaled(elem<kBf16>(row, removed), c) - M) : 0.f;
+  const int removed = s_removed;
+  const float ex = s_ex;
 
   // The chunk holding the target mass: wave 0 takes 64 chunks at a time,
   // scans their masses in chunk order and picks the first chunk whose
@@ -258,7 +290,7 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
   if (tid < kWave) {
     const size_t base = (size_t)r * num_chunks;
     const int rc = removed >= 0 ? removed / kAcceptChunk : -1;
-    const float t = uniforms[2 * (size_t)r + 1] * (s_rz[a] - ex);
+    const float t = s_u1 * (s_rz[a] - ex);
     float carry = 0.f;
     int pick = -1, last = -1, alt = -1;
     float pick_rest = 0.f, last_w = 0.f;
@@ -266,8 +298,9 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
       const int ch = c0 + tid;
       float w = 0.f;
       if (ch < num_chunks) {
-        const float sm = stat_m[base + ch];
-        w = sm == -INFINITY ? 0.f : stat_s[base + ch] * fexp2(sm - M);
+        const float sm = stash ? s_sm[a][ch] : stat_m[base + ch];
+        const float ss = stash ? s_ss[a][ch] : stat_s[base + ch];
+        w = sm == -INFINITY ? 0.f : ss * fexp2(sm - M);
         if (ch == rc) w = fmaxf(w - ex, 0.f);
       }
       const float incl = carry + wave_incl_scan_f(w);
