@@ -358,12 +358,47 @@ struct Share {
   ReqMeta first;  // request i's metadata, as read by the plan
 };
 
-// Computes the share with one block-wide scan over the requests' segment
-// lengths (each thread owns a contiguous run of requests).  Workgroup 0 also
-// publishes the per-request prefix and the share size for the combine kernel.
+// Small batches.  When the even share falls to the minimum, each segment is
+// instead cut into pieces of at most kMinShare keys, as equal as whole
+// blocks allow, one piece per workgroup: no workgroup then pays for a second
+// piece (its metadata, page ids and pipeline refill), which at this size is
+// a large part of the kernel.  Piece q of n of a `seg`-key segment starts at
+// piece_begin(seg, n, q).
+__device__ __forceinline__ int seg_pieces(int seg) { return (seg + kMinShare - 1) / kMinShare; }
+__device__ __forceinline__ int piece_begin(int seg, int n, int q) {
+  return (int)((long long)(seg / kBlockKeys) * q / n) * kBlockKeys;
+}
+
+// Block-wide inclusive scan step of one value per thread: the wave scan,
+// then the wave totals through LDS (`tot` receives the block total).
+__device__ __forceinline__ int block_excl_scan(int v, int *lds_tot, int &tot) {
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  int incl = v;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int y = __shfl_up(incl, d, kWave);
+    if (lane >= d) incl += y;
+  }
+  if (lane == kWave - 1) lds_tot[wave] = incl;
+  __syncthreads();
+  int before = 0;
+  tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    before += w < wave ? lds_tot[w] : 0;
+    tot += lds_tot[w];
+  }
+  return before + incl - v;
+}
+
+// Computes the share with block-wide scans over the requests' segment
+// lengths (each thread owns a contiguous run of requests): a stream-K share
+// of the flattened work, or, for small batches, one piece of one segment.
+// Workgroup 0 also publishes the per-request prefixes and the plan for the
+// combine kernel.  LDS use: lds[0..2*kWaves) scan totals, then the located
+// share.
 __device__ Share plan_share(const AttnParams &p, int *lds) {
   const int B = p.num_reqs, tid = threadIdx.x;
-  const int lane = tid % kWave, wave = tid / kWave;
   const int per = (B + kThreads - 1) / kThreads;
   const int lo = min(B, tid * per), hi = min(B, lo + per);
   int sum = 0;
@@ -381,41 +416,53 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
 #pragma unroll 4
     for (int i = lo; i < hi; ++i) sum += segment_len(p, i);
   }
-  int incl = sum;
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const int y = __shfl_up(incl, d, kWave);
-    if (lane >= d) incl += y;
+  // segment pieces of this thread's requests (for the small-batch plan)
+  int npc = 0;
+  if (per == 1) {
+    npc = seg_pieces(sum);
+  } else {
+    for (int i = lo; i < hi; ++i) npc += seg_pieces(segment_len(p, i));
   }
-  if (lane == kWave - 1) lds[wave] = incl;
-  __syncthreads();
-  int before = 0, total = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    before += w < wave ? lds[w] : 0;
-    total += lds[w];
-  }
-  const int excl = before + incl - sum;  // prefix of this thread's first request
+  int total, total_pc;
+  const int excl = block_excl_scan(sum, lds, total);       // keys before my requests
+  const int excl_pc = block_excl_scan(npc, lds + kWaves, total_pc);
+  int *loc = lds + 2 * kWaves;  // located share: i, g, off, q0, q1, ctx, start, end
   const int work = total * p.hkv;
   int share = (work + (int)gridDim.x - 1) / (int)gridDim.x;
   share = max(kMinShare, round_up_block(share));
-  const int start = (int)blockIdx.x * share;
-  const int end = min(work, start + share);
+  // small batch: the even share is at the minimum and every segment piece
+  // gets a workgroup of its own (uniform: every workgroup computes it)
+  const bool seg_mode = share == kMinShare && total_pc * p.hkv <= (int)gridDim.x;
   if (blockIdx.x == 0) {
-    int acc = excl;
+    int acc = excl, acc_pc = excl_pc;
     for (int i = lo; i < hi; ++i) {
+      const int seg = segment_len(p, i);
       p.plan[i] = acc;
-      acc += segment_len(p, i);
+      p.plan[B + 2 + i] = acc_pc;
+      acc += seg;
+      acc_pc += seg_pieces(seg);
     }
     if (tid == 0) {
       p.plan[B] = total;
-      p.plan[B + 1] = share;
+      p.plan[B + 1] = seg_mode ? 0 : share;  // 0 marks the small-batch plan
+      p.plan[2 * B + 2] = total_pc;
     }
   }
-  // the thread whose requests contain `start` locates it and publishes the
-  // request's metadata, so the first piece needs no second read of it
-  if (start < work && excl * p.hkv <= start && start < (excl + sum) * p.hkv) {
-    int acc = excl;
+  const int b = (int)blockIdx.x;
+  int start = work, end = work;
+  if (!seg_mode) {
+    start = min(work, b * share);
+    end = min(work, start + share);
+  }
+  // the thread whose requests contain this workgroup's share locates it and
+  // publishes the request's metadata, so the first piece needs no second
+  // read of it
+  const bool mine = seg_mode ? (b < total_pc * p.hkv && excl_pc * p.hkv <= b &&
+                                b < (excl_pc + npc) * p.hkv)
+                             : (start < work && excl * p.hkv <= start &&
+                                start < (excl + sum) * p.hkv);
+  if (mine) {
+    int acc = excl, acc_pc = excl_pc;
     for (int i = lo; i < hi; ++i) {
       if (per != 1) {
         q0 = p.cu[i];
@@ -423,35 +470,57 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
         cx = p.ctx[i];
       }
       const int seg = segment_of(p, q0, q1, cx);
-      if (start < (acc + seg) * p.hkv) {
+      const int n = seg_pieces(seg);
+      int g = -1, off = 0, s0 = 0, s1 = 0;
+      if (seg_mode) {
+        if (b < (acc_pc + n) * p.hkv) {
+          const int rel = b - acc_pc * p.hkv;
+          g = rel / n;
+          const int q = rel % n;
+          off = piece_begin(seg, n, q);
+          s0 = acc * p.hkv + g * seg + off;
+          s1 = s0 + piece_begin(seg, n, q + 1) - off;
+        }
+      } else if (start < (acc + seg) * p.hkv) {
         const int rel = start - acc * p.hkv;
-        lds[kWaves + 0] = i;
-        lds[kWaves + 1] = rel / seg;
-        lds[kWaves + 2] = rel % seg;
-        lds[kWaves + 3] = q0;
-        lds[kWaves + 4] = q1;
-        lds[kWaves + 5] = cx;
+        g = rel / seg;
+        off = rel % seg;
+        s0 = start;
+        s1 = end;
+      }
+      if (g >= 0) {
+        loc[0] = i;
+        loc[1] = g;
+        loc[2] = off;
+        loc[3] = q0;
+        loc[4] = q1;
+        loc[5] = cx;
+        loc[6] = s0;
+        loc[7] = s1;
         break;
       }
       acc += seg;
+      acc_pc += n;
     }
   }
   __syncthreads();
   Share sh;
-  sh.start = start;
-  sh.end = end;
-  if (start < work) {
-    sh.i = __builtin_amdgcn_readfirstlane(lds[kWaves + 0]);
-    sh.g = __builtin_amdgcn_readfirstlane(lds[kWaves + 1]);
-    sh.off = __builtin_amdgcn_readfirstlane(lds[kWaves + 2]);
-    const int f0 = __builtin_amdgcn_readfirstlane(lds[kWaves + 3]);
-    const int f1 = __builtin_amdgcn_readfirstlane(lds[kWaves + 4]);
+  const bool has = seg_mode ? b < total_pc * p.hkv : start < work;
+  if (has) {
+    sh.start = __builtin_amdgcn_readfirstlane(loc[6]);
+    sh.end = __builtin_amdgcn_readfirstlane(loc[7]);
+    sh.i = __builtin_amdgcn_readfirstlane(loc[0]);
+    sh.g = __builtin_amdgcn_readfirstlane(loc[1]);
+    sh.off = __builtin_amdgcn_readfirstlane(loc[2]);
+    const int f0 = __builtin_amdgcn_readfirstlane(loc[3]);
+    const int f1 = __builtin_amdgcn_readfirstlane(loc[4]);
     sh.first.q0 = f0;
-    sh.first.ctx = __builtin_amdgcn_readfirstlane(lds[kWaves + 5]);
+    sh.first.ctx = __builtin_amdgcn_readfirstlane(loc[5]);
     sh.first.k = f1 - f0;
     sh.first.len = sh.first.ctx + sh.first.k;
     sh.first.seg = segment_of(p, f0, f1, sh.first.ctx);
   } else {
+    sh.start = sh.end = work;
     sh.i = sh.g = sh.off = 0;
     sh.first = ReqMeta{0, 0, 0, 0, 0};
   }
@@ -539,7 +608,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
   using R = Ring<D>;
   __shared__ __attribute__((aligned(1024))) char ring[kStages * R::kStage];
   __shared__ int pg[kSubPages + 8];
-  __shared__ int lds_plan[kWaves + 6];
+  __shared__ int lds_plan[2 * kWaves + 8];
 
   const Share sh = plan_share(p, lds_plan);
   if (sh.start >= sh.end) return;
@@ -682,7 +751,17 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
   if (seg <= 0) return;
   const int share = p.plan[p.num_reqs + 1];
   const int start = prefix * p.hkv + g * seg;
-  const int b0 = start / share, b1 = (start + seg - 1) / share;
+  int b0, b1;
+  if (share == 0) {
+    // small-batch plan: the segment's n pieces sit on consecutive workgroups,
+    // each the first (and only) piece of its workgroup
+    const int n = seg_pieces(seg);
+    b0 = p.plan[p.num_reqs + 2 + i] * p.hkv + g * n;
+    b1 = b0 + n - 1;
+  } else {
+    b0 = start / share;
+    b1 = (start + seg - 1) / share;
+  }
   if (b0 == b1) return;  // one workgroup held the whole segment
   const int rr = blockIdx.x * kRows + threadIdx.x / kLanesPerRow;
   if (rr >= G * rq.k) return;
@@ -695,7 +774,7 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
   // segment, else slot 1 (the segment is where its share ends)
   auto prow = [&](int u) -> size_t {
     const int b = b0 + u;
-    const int slot = b * share >= start ? 0 : 1;
+    const int slot = share == 0 || b * share >= start ? 0 : 1;
     return ((size_t)b * 2 + slot) * (G * kMaxQlen) + rr;
   };
 
@@ -804,7 +883,7 @@ AttnWorkspace attn_workspace_layout(const dsv_attn_dims &d) {
   const size_t rows = grid * 2 * (size_t)(d.num_q_heads / d.num_kv_heads) * kMaxQlen;
   w.grid_cap = (int32_t)grid;
   w.plan_off = 0;
-  w.part_ml_off = align_up((size_t)(d.num_reqs + 2) * sizeof(int32_t), 256);
+  w.part_ml_off = align_up((size_t)(2 * d.num_reqs + 3) * sizeof(int32_t), 256);
   w.part_o_off = align_up(w.part_ml_off + rows * sizeof(float2), 256);
   w.total = align_up(w.part_o_off + rows * d.head_dim * sizeof(float), 256);
   return w;

@@ -29,7 +29,8 @@ struct AttnParams {
   const int32_t *page_table;  // [B][P_max]
   const int32_t *ctx;         // [B]
   uint16_t *out;              // bf16 [cap][Hq][D]
-  int32_t *plan;              // [B+2]: segment prefix per request, total, share
+  int32_t *plan;              // [2B+3]: key prefix per request, total, share (0 for
+                              // the small-batch plan), piece prefix per request, total
   float2 *part_ml;            // fp32 [grid][2][G*16] x (m, l)   (stream-K partials)
   float *part_o;              // fp32 [grid][2][G*16][D]
   int32_t num_reqs, cap, hq, hkv, group, max_pages, num_pages, max_kv_len;
