@@ -108,6 +108,8 @@ int dsv_verify_attn(const void *q_packed, const int32_t *cu_qlens,
   p.num_pages = dims->num_pages;
   p.max_kv_len = dims->max_kv_len;
   p.num_wg = grid;
+  p.num_cu = attn_num_cu();
+  if (p.num_cu <= 0) return DSV_ERR_HIP;  // device query failed
   p.scale_log2 = dims->scale * 1.4426950408889634f;
   const hipError_t e = launch_verify_attn(p, dims->head_dim, (hipStream_t)hip_stream);
   return e == hipSuccess ? DSV_OK : DSV_ERR_HIP;

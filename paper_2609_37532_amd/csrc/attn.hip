@@ -359,26 +359,43 @@ struct Share {
 };
 
 // Small batches.  When the even share falls to the minimum, each segment is
-// instead cut into pieces of at most kMinShare keys, as equal as whole
-// blocks allow, one piece per workgroup: no workgroup then pays for a second
-// piece (its metadata, page ids and pipeline refill), which at this size is
-// a large part of the kernel.  Piece q of n of a `seg`-key segment starts at
+// instead cut into pieces of at most `cap` keys, as equal as whole blocks
+// allow, one piece per workgroup: no workgroup then pays for a second piece
+// (its metadata, page ids and pipeline refill), which at this size is a
+// large part of the kernel.  The cap is the smallest of kPieceCaps blocks
+// that leaves at most one piece per CU -- a second workgroup on a CU shares
+// its MFMA and LDS with the first and finishes last -- else the smallest,
+// if the pieces fit the grid.  Piece q of n of a `seg`-key segment starts at
 // piece_begin(seg, n, q).
-__device__ __forceinline__ int seg_pieces(int seg) { return (seg + kMinShare - 1) / kMinShare; }
+constexpr int kNumPieceCaps = 5;
+__device__ __forceinline__ int piece_cap(int c) { return (8 + c) * kBlockKeys; }  // 8..12 blocks
+__device__ __forceinline__ int seg_pieces(int seg, int cap) { return (seg + cap - 1) / cap; }
 __device__ __forceinline__ int piece_begin(int seg, int n, int q) {
   return (int)((long long)(seg / kBlockKeys) * q / n) * kBlockKeys;
 }
 
-// Block-wide inclusive scan step of one value per thread: the wave scan,
-// then the wave totals through LDS (`tot` receives the block total).
+// Inclusive prefix sum over the 64 lanes of a wave with DPP row shifts and
+// row broadcasts (lanes without a source add 0): six VALU steps, where a
+// shuffle-based scan would take six LDS permutes.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int dpp_src(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, kCtrl, kRowMask, 0xf, false);
+}
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  v += dpp_src<0x111, 0xf>(v);  // row_shr:1
+  v += dpp_src<0x112, 0xf>(v);  // row_shr:2
+  v += dpp_src<0x114, 0xf>(v);  // row_shr:4
+  v += dpp_src<0x118, 0xf>(v);  // row_shr:8
+  v += dpp_src<0x142, 0xa>(v);  // row_bcast:15
+  v += dpp_src<0x143, 0xc>(v);  // row_bcast:31
+  return v;
+}
+
+// Block-wide exclusive scan of one value per thread: the wave scan, then the
+// wave totals through LDS (`tot` receives the block total).
 __device__ __forceinline__ int block_excl_scan(int v, int *lds_tot, int &tot) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  int incl = v;
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const int y = __shfl_up(incl, d, kWave);
-    if (lane >= d) incl += y;
-  }
+  const int incl = wave_incl_scan(v);
   if (lane == kWave - 1) lds_tot[wave] = incl;
   __syncthreads();
   int before = 0;
@@ -416,23 +433,55 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
 #pragma unroll 4
     for (int i = lo; i < hi; ++i) sum += segment_len(p, i);
   }
-  // segment pieces of this thread's requests (for the small-batch plan)
-  int npc = 0;
-  if (per == 1) {
-    npc = seg_pieces(sum);
-  } else {
-    for (int i = lo; i < hi; ++i) npc += seg_pieces(segment_len(p, i));
-  }
-  int total, total_pc;
-  const int excl = block_excl_scan(sum, lds, total);       // keys before my requests
-  const int excl_pc = block_excl_scan(npc, lds + kWaves, total_pc);
+  int total;
+  const int excl = block_excl_scan(sum, lds, total);  // keys before my requests
   int *loc = lds + 2 * kWaves;  // located share: i, g, off, q0, q1, ctx, start, end
   const int work = total * p.hkv;
   int share = (work + (int)gridDim.x - 1) / (int)gridDim.x;
   share = max(kMinShare, round_up_block(share));
-  // small batch: the even share is at the minimum and every segment piece
-  // gets a workgroup of its own (uniform: every workgroup computes it)
-  const bool seg_mode = share == kMinShare && total_pc * p.hkv <= (int)gridDim.x;
+  // Small batch: the even share is at the minimum.  Count the segment pieces
+  // under every candidate cap (block totals only: one wave sum per cap, one
+  // barrier) and pick the cap; every workgroup computes the same choice.
+  int cap = 0;
+  if (share == kMinShare) {
+    int cnt[kNumPieceCaps];
+#pragma unroll
+    for (int c = 0; c < kNumPieceCaps; ++c) cnt[c] = 0;
+    for (int i = lo; i < hi; ++i) {
+      const int seg = per == 1 ? sum : segment_len(p, i);
+#pragma unroll
+      for (int c = 0; c < kNumPieceCaps; ++c) cnt[c] += seg_pieces(seg, piece_cap(c));
+    }
+    int *red = loc + 8;  // [kNumPieceCaps][kWaves]
+    const int lane = tid % kWave, wave = tid / kWave;
+#pragma unroll
+    for (int c = 0; c < kNumPieceCaps; ++c) {
+      const int v = wave_incl_scan(cnt[c]);
+      if (lane == kWave - 1) red[c * kWaves + wave] = v;
+    }
+    __syncthreads();
+    for (int c = kNumPieceCaps - 1; c >= -1; --c) {
+      // the smallest cap with at most one piece per CU; failing that the
+      // smallest cap if its pieces fit the grid
+      const int cc = c < 0 ? 0 : c;
+      int t = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) t += red[cc * kWaves + w];
+      if (c >= 0 ? t * p.hkv <= p.num_cu : t * p.hkv <= (int)gridDim.x && cap == 0)
+        cap = piece_cap(cc);
+    }
+  }
+  const bool seg_mode = cap > 0;
+  int npc = 0;
+  if (seg_mode) {
+    if (per == 1) {
+      npc = seg_pieces(sum, cap);
+    } else {
+      for (int i = lo; i < hi; ++i) npc += seg_pieces(segment_len(p, i), cap);
+    }
+  }
+  int total_pc;
+  const int excl_pc = block_excl_scan(npc, lds + kWaves, total_pc);
   if (blockIdx.x == 0) {
     int acc = excl, acc_pc = excl_pc;
     for (int i = lo; i < hi; ++i) {
@@ -440,11 +489,11 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
       p.plan[i] = acc;
       p.plan[B + 2 + i] = acc_pc;
       acc += seg;
-      acc_pc += seg_pieces(seg);
+      if (seg_mode) acc_pc += seg_pieces(seg, cap);
     }
     if (tid == 0) {
       p.plan[B] = total;
-      p.plan[B + 1] = seg_mode ? 0 : share;  // 0 marks the small-batch plan
+      p.plan[B + 1] = seg_mode ? -cap : share;  // negative: the small-batch cap
       p.plan[2 * B + 2] = total_pc;
     }
   }
@@ -470,7 +519,7 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
         cx = p.ctx[i];
       }
       const int seg = segment_of(p, q0, q1, cx);
-      const int n = seg_pieces(seg);
+      const int n = seg_mode ? seg_pieces(seg, cap) : 0;
       int g = -1, off = 0, s0 = 0, s1 = 0;
       if (seg_mode) {
         if (b < (acc_pc + n) * p.hkv) {
@@ -608,7 +657,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
   using R = Ring<D>;
   __shared__ __attribute__((aligned(1024))) char ring[kStages * R::kStage];
   __shared__ int pg[kSubPages + 8];
-  __shared__ int lds_plan[2 * kWaves + 8];
+  __shared__ int lds_plan[2 * kWaves + 8 + kNumPieceCaps * kWaves];
 
   const Share sh = plan_share(p, lds_plan);
   if (sh.start >= sh.end) return;
@@ -752,10 +801,10 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
   const int share = p.plan[p.num_reqs + 1];
   const int start = prefix * p.hkv + g * seg;
   int b0, b1;
-  if (share == 0) {
+  if (share <= 0) {
     // small-batch plan: the segment's n pieces sit on consecutive workgroups,
     // each the first (and only) piece of its workgroup
-    const int n = seg_pieces(seg);
+    const int n = seg_pieces(seg, -share);
     b0 = p.plan[p.num_reqs + 2 + i] * p.hkv + g * n;
     b1 = b0 + n - 1;
   } else {
@@ -774,7 +823,7 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
   // segment, else slot 1 (the segment is where its share ends)
   auto prow = [&](int u) -> size_t {
     const int b = b0 + u;
-    const int slot = share == 0 || b * share >= start ? 0 : 1;
+    const int slot = share <= 0 || b * share >= start ? 0 : 1;
     return ((size_t)b * 2 + slot) * (G * kMaxQlen) + rr;
   };
 
@@ -836,6 +885,19 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
   *reinterpret_cast<uint2 *>(p.out + row * D + 4 * d4) = w2;
 }
 
+// Compute units of the current device (cached per device; a host query).
+int device_cus() {
+  static int cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cache[dev] > 0) return cache[dev];
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  cache[dev] = cus;
+  return cus;
+}
+
 // Workgroups the GPU holds at once for the stream-K kernel (cached per
 // device and head dim; a host query, so it is safe during graph capture).
 int resident_workgroups(int head_dim) {
@@ -868,6 +930,8 @@ int32_t attn_grid_cap(const dsv_attn_dims &d) {
                            ((d.max_kv_len + kBlockKeys - 1) / kBlockKeys);
   return (int32_t)(blocks < kMaxGrid ? blocks : kMaxGrid);
 }
+
+int32_t attn_num_cu() { return device_cus(); }
 
 // Launch grid: the workgroups the current device holds at once, capped.
 int32_t attn_grid(const dsv_attn_dims &d) {

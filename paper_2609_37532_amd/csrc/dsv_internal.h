@@ -29,12 +29,14 @@ struct AttnParams {
   const int32_t *page_table;  // [B][P_max]
   const int32_t *ctx;         // [B]
   uint16_t *out;              // bf16 [cap][Hq][D]
-  int32_t *plan;              // [2B+3]: key prefix per request, total, share (0 for
-                              // the small-batch plan), piece prefix per request, total
+  int32_t *plan;              // [2B+3]: key prefix per request, total, share (minus
+                              // the piece cap for the small-batch plan), piece prefix
+                              // per request, total
   float2 *part_ml;            // fp32 [grid][2][G*16] x (m, l)   (stream-K partials)
   float *part_o;              // fp32 [grid][2][G*16][D]
   int32_t num_reqs, cap, hq, hkv, group, max_pages, num_pages, max_kv_len;
   int32_t num_wg;     // persistent grid of the stream-K kernel
+  int32_t num_cu;     // compute units of the device
   float scale_log2;   // softmax scale * log2(e)
 };
 
@@ -45,6 +47,7 @@ struct AttnWorkspace {
 };
 
 int32_t attn_grid(const dsv_attn_dims &d);  // launch grid on the current device
+int32_t attn_num_cu();                      // compute units of the current device
 AttnWorkspace attn_workspace_layout(const dsv_attn_dims &d);
 hipError_t launch_verify_attn(const AttnParams &p, int head_dim, hipStream_t s);
 
