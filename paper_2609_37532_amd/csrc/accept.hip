@@ -47,6 +47,28 @@ __device__ __forceinline__ float elem(const void *row, int v) {
   return ((const float *)row)[v];
 }
 
+// Best (value, index) pair of a wave, in lane 63, with DPP moves instead of
+// shuffles (which compile to LDS permutes): exchanges inside quads, then
+// the half-row and row mirrors, then the row broadcasts.  A lane whose row
+// the broadcast skips keeps its own pair (a no-op take).  `better` is a
+// total order, so the pairing does not change the result.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ void dpp_take(float &bv, int &bi) {
+  const int ov = __builtin_amdgcn_update_dpp(__float_as_int(bv), __float_as_int(bv), kCtrl,
+                                             kRowMask, 0xf, false);
+  const int oi = __builtin_amdgcn_update_dpp(bi, bi, kCtrl, kRowMask, 0xf, false);
+  take(bv, bi, __int_as_float(ov), oi);
+}
+
+__device__ __forceinline__ void wave_best(float &bv, int &bi) {
+  dpp_take<0xB1, 0xf>(bv, bi);   // quad_perm [1,0,3,2]
+  dpp_take<0x4E, 0xf>(bv, bi);   // quad_perm [2,3,0,1]
+  dpp_take<0x141, 0xf>(bv, bi);  // row_half_mirror
+  dpp_take<0x140, 0xf>(bv, bi);  // row_mirror
+  dpp_take<0x142, 0xa>(bv, bi);  // row_bcast:15 into rows 1 and 3
+  dpp_take<0x143, 0xc>(bv, bi);  // row_bcast:31 into rows 2 and 3
+}
+
 // One 16-byte vector starting at element `base` (VEC elements).
 template <bool kBf16>
 __device__ __forceinline__ void take_vec(u32x4 x, int base, float &bv, int &bi) {
@@ -101,22 +123,20 @@ __global__ __launch_bounds__(kThreads) void argmax_chunk_kernel(
       take_vec<kBf16>(__builtin_nontemporal_load(vp + q), vb + q * kVec, bv, bi);
   }
 
-  // wave reduction, then across the four waves through LDS
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) {
-    const float ov = __shfl_xor(bv, m, kWave);
-    const int oi = __shfl_xor(bi, m, kWave);
-    take(bv, bi, ov, oi);
-  }
+  // wave reduction (the result lands in lane 63), then across the four
+  // waves through LDS
+  wave_best(bv, bi);
   __shared__ float sv[kThreads / kWave];
   __shared__ int si[kThreads / kWave];
   const int wave = tid / kWave, lane = tid % kWave;
-  if (lane == 0) {
+  if (lane == kWave - 1) {
     sv[wave] = bv;
     si[wave] = bi;
   }
   __syncthreads();
   if (tid == 0) {
+    bv = sv[0];
+    bi = si[0];
     for (int w = 1; w < kThreads / kWave; ++w) take(bv, bi, sv[w], si[w]);
     best_val[(size_t)r * num_chunks + c] = bv;
     best_idx[(size_t)r * num_chunks + c] = bi;
