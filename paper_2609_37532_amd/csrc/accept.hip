@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kWave) void prefix_kernel(
   const bool mismatch = lane < k - 1 && t != want;
   const unsigned long long mask = __ballot(mismatch);
   const int a = mask ? __builtin_ctzll(mask) : k - 1;
-  const int succ = __shfl(t, a, kWave);
+  const int succ = __builtin_amdgcn_readlane(t, a);  // a is uniform (from the ballot)
   if (lane == 0) {
     accept_len[i] = a;
     next_token[i] = succ;

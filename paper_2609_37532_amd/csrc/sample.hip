@@ -89,6 +89,35 @@ __device__ __forceinline__ void merge(float &m, float &s, float om, float os) {
   }
 }
 
+// (max, sum) merge with a DPP-moved partner instead of a shuffle (which
+// compiles to an LDS permute).  Lanes that the move skips (row broadcasts
+// into masked rows) see the identity (-inf, 0) and stay unchanged.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ void dpp_merge(float &m, float &s) {
+  const float om = __int_as_float(__builtin_amdgcn_update_dpp(
+      __float_as_int(-INFINITY), __float_as_int(m), kCtrl, kRowMask, 0xf, false));
+  const float os = __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(s), kCtrl, kRowMask, 0xf, false));
+  merge(m, s, om, os);
+}
+
+// Merge over each row of 16 lanes (every lane of the row ends with it):
+// exchanges inside quads, then the half-row and row mirrors.
+__device__ __forceinline__ void row16_merge(float &m, float &s) {
+  dpp_merge<0xB1, 0xf>(m, s);   // quad_perm [1,0,3,2]
+  dpp_merge<0x4E, 0xf>(m, s);   // quad_perm [2,3,0,1]
+  dpp_merge<0x141, 0xf>(m, s);  // row_half_mirror
+  dpp_merge<0x140, 0xf>(m, s);  // row_mirror
+}
+
+// Merge over the wave, complete in lane 63: the row merges, then the row
+// broadcasts of lane 15 into rows 1 and 3 and of lane 31 into rows 2 and 3.
+__device__ __forceinline__ void wave_merge(float &m, float &s) {
+  row16_merge(m, s);
+  dpp_merge<0x142, 0xa>(m, s);
+  dpp_merge<0x143, 0xc>(m, s);
+}
+
 template <bool kBf16>
 __device__ __forceinline__ void acc_vec(u32x4 x, float c, float &m, float &s) {
   if (kBf16) {
@@ -160,20 +189,17 @@ __global__ __launch_bounds__(kThreads) void softmax_stats_kernel(
     for (int q = tid; q < nvec; q += kThreads)
       acc_vec<kBf16>(__builtin_nontemporal_load(vp + q), c, m, s);
   }
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const float om = __shfl_xor(m, d, kWave);
-    const float os = __shfl_xor(s, d, kWave);
-    merge(m, s, om, os);
-  }
+  wave_merge(m, s);  // complete in lane 63
   __shared__ float sm[kThreads / kWave], ss[kThreads / kWave];
   const int wave = tid / kWave, lane = tid % kWave;
-  if (lane == 0) {
+  if (lane == kWave - 1) {
     sm[wave] = m;
     ss[wave] = s;
   }
   __syncthreads();
   if (tid == 0) {
+    m = sm[0];
+    s = ss[0];
     for (int w = 1; w < kThreads / kWave; ++w) merge(m, s, sm[w], ss[w]);
     stat_m[(size_t)r * num_chunks + ch] = m;
     stat_s[(size_t)r * num_chunks + ch] = s;
@@ -243,12 +269,7 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
         merge(m, s, cm, cs);
       }
     }
-#pragma unroll
-    for (int d = 8; d >= 1; d >>= 1) {
-      const float om = __shfl_xor(m, d, 16);
-      const float os = __shfl_xor(s, d, 16);
-      merge(m, s, om, os);
-    }
+    row16_merge(m, s);
     if (j < k && l == 0) {
       s_rm[j] = m;
       s_rz[j] = s;
@@ -308,17 +329,19 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
       const unsigned long long other = __ballot(w > 0.f && ch != rc);
       if (pos) {
         last = c0 + 63 - __builtin_clzll(pos);
-        last_w = __shfl(w, 63 - __builtin_clzll(pos), kWave);
+        last_w = __int_as_float(
+            __builtin_amdgcn_readlane(__float_as_int(w), 63 - __builtin_clzll(pos)));
       }
       if (other) alt = c0 + 63 - __builtin_clzll(other);
       const unsigned long long hit = __ballot(w > 0.f && incl > t);
       if (pick < 0 && hit) {
         const int l = __builtin_ctzll(hit);
-        const float before = l > 0 ? __shfl(incl, l - 1, kWave) : carry;
+        const float before =
+            l > 0 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(incl), l - 1)) : carry;
         pick = c0 + l;
         pick_rest = t - before;
       }
-      carry = __shfl(incl, kWave - 1, kWave);
+      carry = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(incl), kWave - 1));
       if (pick >= 0) break;  // uniform: every lane saw the same ballot
     }
     if (pick < 0) {  // the uniform at or past the rounded total
