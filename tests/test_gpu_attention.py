@@ -92,6 +92,17 @@ def test_many_requests(B):
     check(case(B + 11, ctx, k, hq=8, hkv=2, d=64, max_kv_len=416), "many-requests-%d" % B)
 
 
+@pytest.mark.parametrize("name,ctx,qlens", [
+    # one long request: the small-batch plan cuts its 8 segments into about
+    # 30 pieces each (a piece cap above 8 blocks to stay within one per CU),
+    # so the combine merges far more than 8 partials per row
+    ("one-long-request", [8000], [16]),
+    ("two-requests-one-long", [7000, 40], [9, 16]),
+])
+def test_small_batch_many_pieces(name, ctx, qlens):
+    check(case(zlib.crc32(name.encode()) % 1000, ctx, qlens, max_kv_len=8016), name)
+
+
 def test_long_context():
     check(case(77, [16000, 9000, 31], [4, 16, 2], max_kv_len=16384), "long-context")
 
