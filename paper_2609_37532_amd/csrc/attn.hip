@@ -22,7 +22,9 @@
 //    contexts cost no idle workgroups, and there are at most two partials
 //    per workgroup.  Results depend only on the request's own data and the
 //    batch's total work (the share size), and merge in a fixed order, so
-//    they are deterministic.
+//    they are deterministic.  Small batches, whose even share would fall
+//    below eight blocks, instead cut every segment into equal block-aligned
+//    pieces, one per workgroup, so that no workgroup straddles two segments.
 //  * K/V stream through an LDS ring of three 32-key blocks.  Each wave
 //    loads one 4 KiB tile per block (one page's K or V) into registers
 //    three blocks ahead, as four contiguous 1 KiB loads from a scalar page
@@ -460,6 +462,8 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
       if (lane == kWave - 1) red[c * kWaves + wave] = v;
     }
     __syncthreads();
+    // every piece needs a workgroup of the grid
+    const int one_per_cu = min(p.num_cu, (int)gridDim.x);
     for (int c = kNumPieceCaps - 1; c >= -1; --c) {
       // the smallest cap with at most one piece per CU; failing that the
       // smallest cap if its pieces fit the grid
@@ -467,7 +471,7 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
       int t = 0;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) t += red[cc * kWaves + w];
-      if (c >= 0 ? t * p.hkv <= p.num_cu : t * p.hkv <= (int)gridDim.x && cap == 0)
+      if (c >= 0 ? t * p.hkv <= one_per_cu : t * p.hkv <= (int)gridDim.x && cap == 0)
         cap = piece_cap(cc);
     }
   }
