@@ -369,13 +369,39 @@ __global__ __launch_bounds__(kThreads) void stochastic_prefix_kernel(
     const int ch = s_chunk;
     const float t = s_target;
     const int v0 = ch * kAcceptChunk + tid * kPerThread;
+    // this thread's run of logits: 16-byte vector loads when the run is
+    // whole and aligned (rows of a vocabulary that is a multiple of 8), else
+    // element by element
+    float x[kPerThread];
+    const char *run = row + (size_t)v0 * kEs;
+    if (v0 + kPerThread <= vocab && ((uintptr_t)run & 15) == 0) {
+      constexpr int kVecs = kPerThread * kEs / 16;
+      u32x4 w[kVecs];
+#pragma unroll
+      for (int u = 0; u < kVecs; ++u) w[u] = reinterpret_cast<const u32x4 *>(run)[u];
+#pragma unroll
+      for (int u = 0; u < kVecs; ++u)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (kBf16) {
+            x[8 * u + 2 * q] = bf16_lo(w[u][q]);
+            x[8 * u + 2 * q + 1] = bf16_hi(w[u][q]);
+          } else {
+            x[4 * u + q] = __uint_as_float(w[u][q]);
+          }
+        }
+    } else {
+#pragma unroll
+      for (int q = 0; q < kPerThread; ++q)
+        x[q] = v0 + q < vocab ? elem<kBf16>(row, v0 + q) : 0.f;
+    }
     float e[kPerThread];
     float mine = 0.f;
 #pragma unroll
     for (int q = 0; q < kPerThread; ++q) {
       const int v = v0 + q;
       float ev = 0.f;
-      if (v < vocab && v != removed) ev = fexp2(scaled(elem<kBf16>(row, v), c) - M);
+      if (v < vocab && v != removed) ev = fexp2(scaled(x[q], c) - M);
       e[q] = ev;
       mine += ev;
     }
