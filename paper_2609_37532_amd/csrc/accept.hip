@@ -10,7 +10,7 @@
 // How: the logits stream is the whole cost (2 bytes per element at bf16),
 // so the argmax runs on (vocabulary chunk x row) workgroups, each streaming
 // 16 KiB with 16-byte coalesced loads issued back to back, reducing
-// (value, index) pairs inside the wave with xor shuffles and across the
+// (value, index) pairs inside the wave with DPP moves and across the
 // four waves in LDS, and writing one pair per (row, chunk).  No atomics: a
 // second kernel, one wave per request, reduces the chunk pairs in a fixed
 // order and does the prefix compare with a ballot.  The comparison is exact
