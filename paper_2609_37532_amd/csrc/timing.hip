@@ -63,8 +63,13 @@ int dsv_timing_start(int32_t max_launches) {
   t.start.resize(max_launches);
   t.stop.resize(max_launches);
   t.kind.assign(max_launches, -1);
+  // Timing-only events: recording them does no system-scope fence, so the
+  // interval does not include a writeback and invalidation of the caches
+  // (the kernel's own end-of-dispatch release is still inside it).
+  constexpr unsigned kFlags = hipEventDisableSystemFence;
   for (int n = 0; n < max_launches; ++n) {
-    if (hipEventCreate(&t.start[n]) != hipSuccess || hipEventCreate(&t.stop[n]) != hipSuccess) {
+    if (hipEventCreateWithFlags(&t.start[n], kFlags) != hipSuccess ||
+        hipEventCreateWithFlags(&t.stop[n], kFlags) != hipSuccess) {
       t.start.resize(n);
       t.stop.resize(n);
       release(t);
