@@ -74,6 +74,20 @@ def test_sentinels_and_tail():
     check(inp, "sentinels")
 
 
+def test_all_sentinels_zero_every_row():
+    # no live row at all: the plan has no work, every attention workgroup
+    # exits at once, and the combine still zeroes all capacity rows
+    inp = case(6, [300, 0, 17, 2000], [0, 0, 0, 0], cap=24)
+    got = check(inp, "all-sentinels")
+    assert not got.any()
+
+
+def test_live_rows_fill_capacity():
+    # no tail: the last request's rows end exactly at the capacity
+    qlens = [16, 1, 9, 16, 4]
+    check(case(8, [700, 3, 95, 1500, 64], qlens, cap=sum(qlens)), "no-tail")
+
+
 @pytest.mark.parametrize("hq,hkv,d", [(4, 4, 128), (8, 4, 64), (16, 2, 128), (16, 1, 64),
                                       (32, 8, 64)])
 def test_head_layouts(hq, hkv, d):
