@@ -207,3 +207,56 @@ def test_prefix_stability_within_tolerance():
                            scale=base.scale)
         got = run_attn(alt)
         assert np.abs(got[:k] - full[:k]).max() <= 2.0 ** -7
+
+
+# ------------------------------------------------------------ random sweep
+def sweep_case(seed):
+    """A seeded random batch: head layout, batch size, context distribution,
+    verify lengths (with sentinels), capacity slack.  Contexts are redrawn
+    shorter until the oracle's work stays near a second.  The kind cycles
+    with the seed so both plans are reached: small batches cut whole
+    segments into pieces, and the last kind (many KV heads, few query rows,
+    long contexts) always takes stream-K shares that straddle segments."""
+    rng = np.random.default_rng(10_000 + seed)
+    kind = seed % 5
+    G = int(rng.choice([1, 2, 4, 8, 16]))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    while G * hkv > 64:
+        hkv //= 2
+    d = int(rng.choice([64, 128]))
+    B = int(rng.choice([1, 2, 3, 5, 8, 13, 24, 40, 96, 300]))
+    kmax = 17
+    if kind == 4:
+        G, hkv, d = int(rng.choice([1, 2])), 8, 64
+        B, kmax = int(rng.choice([24, 40, 96])), 5
+    k = rng.integers(1, kmax, size=B)
+    k[rng.random(B) < 0.15] = 0
+    hi = 4000
+    while True:
+        if kind == 0:    # uniform
+            ctx = rng.integers(0, hi, size=B)
+        elif kind == 1:  # ctx + k on or next to 32-key block edges
+            ctx = np.maximum(0, 32 * rng.integers(0, hi // 32, size=B) - k
+                             + rng.integers(-1, 2, size=B))
+        elif kind == 2:  # one long request among short ones
+            ctx = rng.integers(0, 64, size=B)
+            ctx[int(rng.integers(0, B))] = int(rng.integers(hi // 2, hi))
+        elif kind == 3:  # short contexts only
+            ctx = rng.integers(0, 48, size=B)
+        else:            # long contexts
+            ctx = rng.integers(hi // 4, hi, size=B)
+        work = float(np.sum(k.astype(np.float64) * G * hkv * (ctx + k) * d))
+        if work <= 4e8 or hi <= 64:
+            break
+        hi //= 2
+    cap = int(k.sum()) + int(rng.integers(0, 24))
+    return dict(seed=seed, ctx=ctx, qlens=k, cap=max(cap, 1), hq=G * hkv, hkv=hkv, d=d,
+                max_kv_len=int((ctx + k).max()) + int(rng.integers(0, 40)))
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_random_sweep(seed):
+    c = sweep_case(seed)
+    check(case(c["seed"], c["ctx"], c["qlens"], cap=c["cap"], hq=c["hq"], hkv=c["hkv"],
+               d=c["d"], max_kv_len=max(c["max_kv_len"], 1)),
+          "sweep-%d hq=%d hkv=%d d=%d" % (seed, c["hq"], c["hkv"], c["d"]))
