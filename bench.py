@@ -425,6 +425,66 @@ def bucket_bench(layers=4, reps=5):
                                   for m in mem["buckets"]]}
 
 
+READ_PROBE_GRIDS = (512, 1024, 2048, 4096)
+
+
+def read_ceiling(stream, pool_gib=4, reps=10):
+    """The read rate scattered 4 KiB page tiles reach on this device, the
+    ceiling the attention kernel is compared with beside the vendor peak.
+    ``read_probe`` reads every tile of a 4 GiB pool once per launch in a
+    seeded random order, alternating between two pools so that no launch
+    finds the previous one's tiles in the 256 MB Infinity Cache; HIP events
+    bracket ``reps`` launches per grid size, and the best grid is reported.
+    Three orders: random tiles, random 64 KiB pages with their tiles in
+    sequence, and address order.  ``peak_gbps`` is the highest of the three,
+    the measured read peak."""
+    import torch
+
+    import paper_2609_37532_amd as dsv
+    import workloads as W
+    dev = torch.device("cuda", 0)
+    n_tiles = pool_gib << 18
+    nbytes = n_tiles * 4096
+    pools = [torch.empty(nbytes, dtype=torch.uint8, device=dev) for _ in range(2)]
+    for k, pool in enumerate(pools):
+        pool.fill_(0x3c + k)
+    gen = torch.Generator()
+    gen.manual_seed(W.SEED_BASE + 77)
+    pages = torch.randperm(n_tiles // 16, generator=gen).to(torch.int32)
+    orders = {
+        # every 4 KiB tile in a random order
+        "random_tiles": torch.randperm(n_tiles, generator=gen).to(torch.int32).to(dev),
+        # 64 KiB pages (16 tiles, one page of all eight KV heads' K or V) in a
+        # random order, the tiles of a page one after another
+        "random_pages": (pages[:, None] * 16 + torch.arange(16, dtype=torch.int32)).reshape(-1)
+        .to(dev),
+        "address_order": torch.arange(n_tiles, dtype=torch.int32, device=dev),
+    }
+    out = {"pool_bytes": nbytes, "tile_bytes": 4096, "kernel": "read_probe_kernel",
+           "timing": "HIP events around %d launches per grid size, two pools alternating" % reps}
+    with torch.cuda.stream(stream):
+        for name, order in orders.items():
+            per_grid = {}
+            for grid in READ_PROBE_GRIDS:
+                sink = torch.empty(grid, dtype=torch.int32, device=dev)
+                for r in range(2):
+                    dsv.read_probe(pools[r % 2], order, sink, stream=stream)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for r in range(reps):
+                    dsv.read_probe(pools[r % 2], order, sink, stream=stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                per_grid[str(grid)] = round(nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+            best = max(per_grid, key=per_grid.get)
+            out[name] = {"gbps": per_grid[best], "grid": int(best), "per_grid_gbps": per_grid}
+    out["peak_gbps"] = max(out[name]["gbps"] for name in orders)
+    del pools, orders
+    torch.cuda.empty_cache()
+    return out
+
+
 def copy_probe():
     """Three device-to-device copies of 1 GiB: reads and writes 2^30 bytes
     each, the known size against which FETCH_SIZE / WRITE_SIZE are scaled."""
@@ -589,6 +649,12 @@ def main():
         "combine_us": round(t_comb * 1e6, 2),
     }
     graph.close()
+
+    log("read ceiling ...")
+    ceiling = read_ceiling(stream)
+    result["read_ceiling"] = ceiling
+    result["roofline"]["measured_read_peak"] = ceiling["peak_gbps"]
+    result["roofline"]["frac_of_measured_peak"] = round(achieved / ceiling["peak_gbps"], 4)
 
     log("configs 2-4 attention ...")
     result["attention_configs"] = configs_bench()

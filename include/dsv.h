@@ -367,11 +367,38 @@ int dsv_graph_replay(void *graph_exec, void *hip_stream);
 int dsv_graph_destroy(void *graph_exec);
 
 /*
+ * Read-rate probe for measurement harnesses; not part of the verify path.
+ * Reads `visits` tiles of 4096 bytes from `buf`, tile order[v] at visit v,
+ * with 16-byte loads.  A 4 KiB tile is what the verify attention reads per
+ * page and KV head (16 tokens x D = 128 x bf16), so a random order over a
+ * pool larger than the 256 MB Infinity Cache measures the read rate that
+ * scattered page tiles reach, the ceiling the attention is compared with.
+ *
+ *   buf        device, 16-byte aligned, buf_tiles * 4096 bytes.
+ *   order      device int32 [visits]; an id outside [0, buf_tiles) is read
+ *              as nothing (contributes 0).
+ *   sink       device uint32 [grid]; workgroup b reads visits
+ *              [b*per, (b+1)*per), per = ceil(visits / grid), twelve tiles
+ *              in flight at a time, and writes the XOR of every 32-bit word
+ *              it read to sink[b].
+ *   grid       workgroups of 256 threads, 1 .. 65535.
+ *
+ * Asynchronous on hip_stream; no allocation.  Returns DSV_ERR_NULL,
+ * DSV_ERR_DIMS (buf_tiles, visits or grid out of range), DSV_ERR_UNSUPPORTED
+ * (buf not 16-byte aligned) or DSV_ERR_HIP (launch failed).
+ */
+int dsv_read_probe(const void *buf, int32_t buf_tiles, const int32_t *order,
+                   int32_t visits, uint32_t *sink, int32_t grid, void *hip_stream);
+
+/*
  * Kernel timing for measurement harnesses.  After dsv_timing_start(n), the
  * next n kernel launches made by eager (not captured) dsv_verify_attn,
  * dsv_accept, dsv_accept_stochastic, dsv_predictor_forward and
  * dsv_dvl_allocate_pack calls are bracketed by HIP events
- * recorded on the caller's stream.  dsv_timing_stop waits for those events,
+ * recorded on the caller's stream.  The events are timing-only (created
+ * with hipEventDisableSystemFence): recording them performs no system-scope
+ * cache writeback or invalidation, so an interval covers the kernel and
+ * not such a fence.  dsv_timing_stop waits for those events,
  * writes per kernel kind the summed milliseconds and the launch count (arrays
  * of DSV_TIMING_KINDS), and turns timing off.  Kinds: 0 attention split
  * kernel, 1 attention combine kernel, 2 vocabulary argmax kernel,

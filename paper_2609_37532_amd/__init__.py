@@ -18,7 +18,8 @@ verify graphs for a set of request-bucket sizes (``select_bucket``).
 
 This module only marshals arguments; PyTorch provides device memory and
 streams.  ``Graph`` captures and replays the calls with fixed buffer
-addresses; ``KernelTimer`` times the kernels with HIP events.
+addresses; ``KernelTimer`` times the kernels with HIP events, and
+``read_probe`` measures the read rate of scattered 4 KiB tiles.
 """
 from ._lib import (  # noqa: F401
     DSV_BF16,
@@ -43,6 +44,7 @@ from ._lib import (  # noqa: F401
     predictor_forward,
     predictor_workspace_bytes,
     load,
+    read_probe,
     status_string,
     validate_metadata,
     verify_attn,

@@ -74,6 +74,7 @@ def load():
         "dsv_graph_capture_end": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_void_p)]),
         "dsv_graph_replay": (ctypes.c_int, [P, P]),
         "dsv_graph_destroy": (ctypes.c_int, [P]),
+        "dsv_read_probe": (ctypes.c_int, [P, I32, P, I32, P, I32, P]),
         "dsv_timing_start": (ctypes.c_int, [I32]),
         "dsv_timing_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_float),
                                            ctypes.POINTER(ctypes.c_int32)]),
@@ -315,6 +316,27 @@ def dvl_allocate_pack(pred_logits, num_live, tokens, positions, kv_refs, k_out, 
         _ptr(pred_logits), _ptr(num_live), _ptr(tokens), _ptr(positions), _ptr(kv_refs),
         _ptr(k_out), _ptr(cu_qlens), _ptr(packed_tokens), _ptr(packed_positions),
         _ptr(packed_kv_refs), _ptr(scores_out), n_bs, w, _stream_handle(stream)))
+
+
+
+PROBE_TILE_BYTES = 4096
+
+
+def read_probe(buf, order, sink, *, stream=None) -> None:
+    """Read-rate probe (not part of the verify path): reads the 4 KiB tiles
+    of ``buf`` that ``order`` names, one workgroup per entry of ``sink``,
+    which receives the XOR of the 32-bit words each workgroup read."""
+    import torch
+    _require(buf, "buf", (torch.uint8, torch.int32, torch.float32, torch.bfloat16,
+                          torch.float16, torch.int64), 1)
+    nbytes = buf.numel() * buf.element_size()
+    if nbytes % PROBE_TILE_BYTES or nbytes // PROBE_TILE_BYTES >= 2 ** 31:
+        raise ValueError("buf must hold a whole number of 4096-byte tiles (< 2^31 of them)")
+    _require(order, "order", (torch.int32,), 1)
+    _require(sink, "sink", (torch.int32,), 1)
+    _check("dsv_read_probe", load().dsv_read_probe(
+        _ptr(buf), nbytes // PROBE_TILE_BYTES, _ptr(order), order.numel(), _ptr(sink),
+        sink.numel(), _stream_handle(stream)))
 
 
 class Graph:

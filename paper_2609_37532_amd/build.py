@@ -13,7 +13,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libdsv.so")
-SOURCES = ["abi.hip", "attn.hip", "accept.hip", "sample.hip", "predictor.hip", "dvl.hip", "timing.hip"]
+SOURCES = ["abi.hip", "attn.hip", "accept.hip", "sample.hip", "predictor.hip", "dvl.hip", "timing.hip", "probe.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -203,3 +203,17 @@ def test_predictor_rejects_bad_arguments():
     assert lib.dsv_predictor_forward(*bad) == -3
     bad = list(args); bad[12] = need - 1
     assert lib.dsv_predictor_forward(*bad) == -4
+
+
+def test_read_probe_argument_errors():
+    # every one of these is rejected on the host, before any launch
+    lib = dsv.load()
+    fake = 1 << 20
+    assert lib.dsv_read_probe(None, 4, fake, 4, fake, 1, None) == -1
+    assert lib.dsv_read_probe(fake, 4, None, 4, fake, 1, None) == -1
+    assert lib.dsv_read_probe(fake, 4, fake, 4, None, 1, None) == -1
+    assert lib.dsv_read_probe(fake, 0, fake, 4, fake, 1, None) == -2
+    assert lib.dsv_read_probe(fake, 4, fake, 0, fake, 1, None) == -2
+    assert lib.dsv_read_probe(fake, 4, fake, 4, fake, 0, None) == -2
+    assert lib.dsv_read_probe(fake, 4, fake, 4, fake, 65536, None) == -2
+    assert lib.dsv_read_probe(fake + 8, 4, fake, 4, fake, 1, None) == -3
