@@ -267,7 +267,8 @@ int dsv_validate_metadata(const int32_t *cu_qlens, const int32_t *ctx_lens,
  *   h = relu(features_i . W1 + b1),   pred_logits_i = h . W2 + b2,
  * a perceptron with one ReLU hidden layer of DSV_PRED_HIDDEN units (the
  * paper's 1735 -> 64 -> 15, 112,079 parameters).  Rows i >= N of
- * pred_logits are written as 0; their features are not read.
+ * pred_logits are written as 0; their features are not used (any values,
+ * NaN included: the rows lie inside the buffer and may be loaded).
  *
  *   features     fp32 [N_bs][in_dim], device.
  *   W1 [in_dim][64], b1 [64], W2 [64][out_dim], b2 [out_dim]: fp32, row-major,

@@ -80,13 +80,15 @@ def check(d: W.PredictorInputs, name):
 
 
 @pytest.mark.parametrize("n_bs,n_live,seed", [(1, 1, 0), (32, 32, 1), (100, 77, 2),
-                                              (256, 256, 3), (1024, 1000, 4), (64, 0, 5)])
+                                              (256, 256, 3), (1024, 1000, 4), (64, 0, 5),
+                                              (8, 8, 6), (16, 11, 7), (24, 20, 8)])
 def test_parity_paper_shape(n_bs, n_live, seed):
     d = W.make_predictor_inputs(np.random.default_rng(9000 + seed), n_bs=n_bs, n_live=n_live)
     check(d, "paper shape")
 
 
-@pytest.mark.parametrize("dims", [(5, 64, 3), (64, 64, 15), (65, 64, 1), (4000, 64, 40)])
+@pytest.mark.parametrize("dims", [(5, 64, 3), (64, 64, 15), (65, 64, 1), (4000, 64, 40),
+                                  (300, 64, 100)])
 def test_parity_other_shapes(dims):
     d = W.make_predictor_inputs(np.random.default_rng(9100 + dims[0]), n_bs=70, n_live=66,
                                 dims=dims)
