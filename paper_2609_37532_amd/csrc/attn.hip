@@ -681,8 +681,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
   c.rl = ring_lane<D>(lane);
 
   int i = sh.i, g = sh.g, off = sh.off, pos = sh.start, piece = 0;
+  // metadata of the request last read: the next KV head's segment of the
+  // same request (the usual next piece) needs no second read of it
+  int i_meta = sh.i;
+  ReqMeta meta = sh.first;
   while (pos < sh.end && i < p.num_reqs) {
-    const ReqMeta rq = piece == 0 && i == sh.i ? sh.first : load_req(p, i);
+    if (i != i_meta) {
+      meta = load_req(p, i);
+      i_meta = i;
+    }
+    const ReqMeta rq = meta;
     if (rq.seg == 0) {  // sentinel or bad metadata: no keys in the plan
       ++i;
       continue;
