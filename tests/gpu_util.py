@@ -66,13 +66,27 @@ def attn_errors(got: np.ndarray, ref: np.ndarray, inp: W.AttnInputs):
     return float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
 
 
+def attn_bound(ref, max_abs=1e-2):
+    """Per-element bound on |out - oracle|: max_abs, except where the bf16
+    output format cannot meet it.  The output is rounded once to bf16
+    (nearest even), which moves an element of magnitude |r| by up to
+    2^-8 |r|, more than 1e-2 from |r| ~ 2.56 up; there the bound is that
+    rounding plus 2e-3 for the arithmetic.  Below |r| ~ 2 it is max_abs."""
+    return np.maximum(max_abs, 2.0 ** -8 * np.abs(ref) + 2e-3)
+
+
 def assert_attn_close(got, ref, inp, max_abs=1e-2, mean_abs=1e-3):
-    """Tolerance of the verify path: max-abs 1e-2, mean-abs 1e-3 vs fp64;
+    """Tolerance of the verify path vs fp64: every live element within
+    attn_bound (max-abs 1e-2 wherever bf16 can hold it), mean-abs 1e-3;
     tail rows exactly zero."""
     live = int(inp.cu_qlens[-1])
     assert np.isfinite(got).all(), "non-finite output"
     mx, mn = attn_errors(got, ref, inp)
-    assert mx <= max_abs and mn <= mean_abs, "max %.3g mean %.3g" % (mx, mn)
+    err = np.abs(got[:live] - ref[:live])
+    over = err - attn_bound(ref[:live], max_abs)
+    worst = float(over.max()) if over.size else -1.0
+    assert worst <= 0 and mn <= mean_abs, "max %.3g mean %.3g (worst excess over the bound %.3g)" % (
+        mx, mn, worst)
     assert not got[live:].any(), "tail rows not zero"
     return mx, mn
 

@@ -1,6 +1,7 @@
 """GPU parity of dsv_verify_attn against the fp64 oracle (through the C ABI).
 
-Bar: max-abs error <= 1e-2 and mean-abs error <= 1e-3 over live rows, tail
+Bar: max-abs error <= 1e-2 (or, where the bf16 output cannot hold that,
+2^-8 |oracle| + 2e-3) and mean-abs error <= 1e-3 over live rows, tail
 rows exactly zero, every output finite although every element the kernel
 must not read is NaN (tail q rows, dead slots of last pages, spare pages).
 Invariants that the design makes exact are checked bitwise (page
@@ -115,6 +116,26 @@ def test_many_requests(B):
 ])
 def test_small_batch_many_pieces(name, ctx, qlens):
     check(case(zlib.crc32(name.encode()) % 1000, ctx, qlens, max_kv_len=8016), name)
+
+
+def test_large_outputs_bf16_bound():
+    # Many very short contexts at G = 16: with a handful of keys an output
+    # reaches |x| > 4, where rounding to bf16 alone moves it by up to 0.0156.
+    # The flat 1e-2 is then out of reach for any bf16 output (the oracle's
+    # own bf16 rounding breaks it here); the bound takes the format into
+    # account there and stays 1e-2 below |x| ~ 2.
+    import torch
+    from gpu_util import attn_bound
+    c = sweep_case(111)
+    inp = case(c["seed"], c["ctx"], c["qlens"], cap=c["cap"], hq=c["hq"], hkv=c["hkv"],
+               d=c["d"], max_kv_len=max(c["max_kv_len"], 1))
+    ref = oracle_out(inp)
+    live = int(inp.cu_qlens[-1])
+    r = ref[:live]
+    rounded = torch.from_numpy(r.astype(np.float32)).to(torch.bfloat16).double().numpy()
+    assert np.abs(rounded - r).max() > 1e-2  # the flat bound is unattainable here
+    assert (np.abs(rounded - r) <= attn_bound(r)).all()  # the format-aware one is not
+    check(inp, "large-outputs")
 
 
 def test_long_context():
