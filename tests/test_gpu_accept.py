@@ -142,3 +142,27 @@ def test_one_workspace_across_calls():
         ra, rn = oracle.accept(acc.logits, acc.dtype, acc.cu_qlens, acc.draft_tokens)
         assert np.array_equal(a_dev.cpu().numpy(), ra), call
         assert np.array_equal(n_dev.cpu().numpy(), rn), call
+
+
+def accept_sweep_case(seed):
+    """A seeded random batch: request count, verify lengths with sentinels,
+    capacity slack, vocabulary size (odd sizes misalign rows), dtype and the
+    planted acceptance rate."""
+    rng = np.random.default_rng(60_000 + seed)
+    B = int(rng.choice([1, 2, 5, 16, 32, 33, 64, 200, 300]))
+    k = rng.integers(0, 17, size=B).astype(np.int32)
+    k[rng.random(B) < 0.1] = 0
+    cu = W.cu_from_lengths(k)
+    cap = int(cu[-1]) + int(rng.integers(0, 20)) + 1
+    vocab = int(rng.choice([2, 3, 17, 999, 8191, 8192, 8193, 32000, 151936, 262144])
+                + (rng.integers(0, 9) if rng.random() < 0.3 else 0))
+    dtype = "bf16" if rng.random() < 0.6 else "f32"
+    if cap * vocab > 60_000_000:
+        vocab = max(2, 60_000_000 // cap)
+    return W.make_accept_inputs(rng, cu_qlens=cu, capacity=cap, vocab=vocab, dtype=dtype,
+                                p_accept=float(rng.uniform(0.05, 0.95)))
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_sweep(seed):
+    check(accept_sweep_case(seed), "sweep%d" % seed)

@@ -169,3 +169,23 @@ def test_graph_replay_with_changing_inputs():
             compare(dev.result(), expected(d), "graph%d" % step)
     finally:
         g.close()
+
+
+def dvl_sweep_case(seed):
+    """A seeded random bucket: size, live count, block width, tied logits and
+    the acceptance-rate range (low rates make long grow loops, high rates
+    long shrink loops)."""
+    rng = np.random.default_rng(50_000 + seed)
+    n_bs = int(rng.choice([1, 2, 3, 8, 16, 31, 32, 33, 64, 100, 255, 256, 500, 1024]))
+    n_live = int(rng.integers(0, n_bs + 1)) if rng.random() < 0.5 else n_bs
+    width = int(rng.choice([2, 4, 6, 8, 10, 12, 14, 16, 16, 16]))
+    ties = bool(rng.random() < 0.4)
+    lo = float(rng.uniform(0.2, 0.95))
+    hi = float(min(0.999, lo + rng.uniform(0.01, 0.3)))
+    return W.make_dvl_inputs(rng, n_bs=n_bs, n_live=n_live, width=width, ties=ties,
+                             rate_range=(lo, hi))
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_sweep(seed):
+    check(dvl_sweep_case(seed), "sweep%d" % seed)
