@@ -805,19 +805,31 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
     }
     return;
   }
-  // the request's metadata is read together with the plan (one round trip)
-  const ReqMeta rq = load_req(p, i);
-  const int prefix = p.plan[i];
-  const int seg = p.plan[i + 1] - prefix;  // p.plan[B] is the total
+  // Every plan entry and metadata word this workgroup may need, loaded in
+  // one round trip: the empty asm uses them all before the first branch,
+  // so the compiler cannot sink the loads that one path needs behind the
+  // branches (which made a chain of dependent round trips).
+  int prefix = p.plan[i], next = p.plan[i + 1];  // p.plan[B] is the total
+  int share = p.plan[p.num_reqs + 1];
+  int pc_prefix = p.plan[p.num_reqs + 2 + i];  // read by the small-batch plan only
+  int cq0 = p.cu[i], cq1 = p.cu[i + 1], cctx = p.ctx[i];
+  asm volatile("" : "+s"(prefix), "+s"(next), "+s"(share), "+s"(pc_prefix), "+s"(cq0),
+               "+s"(cq1), "+s"(cctx));
+  ReqMeta rq;
+  rq.q0 = cq0;
+  rq.ctx = cctx;
+  rq.k = cq1 - cq0;
+  rq.len = cctx + rq.k;
+  rq.seg = segment_of(p, cq0, cq1, cctx);
+  const int seg = next - prefix;
   if (seg <= 0) return;
-  const int share = p.plan[p.num_reqs + 1];
   const int start = prefix * p.hkv + g * seg;
   int b0, b1;
   if (share <= 0) {
     // small-batch plan: the segment's n pieces sit on consecutive workgroups,
     // each the first (and only) piece of its workgroup
     const int n = seg_pieces(seg, -share);
-    b0 = p.plan[p.num_reqs + 2 + i] * p.hkv + g * n;
+    b0 = pc_prefix * p.hkv + g * n;
     b1 = b0 + n - 1;
   } else {
     b0 = start / share;
