@@ -13,9 +13,11 @@
 //    serves all G heads (GQA sharing) and a request never pays for rows it
 //    does not have (Eq. (2)'s padding applies per 16-row tile, not per 128).
 //  * Stream-K work split.  Each (request, KV head) pair is a segment of
-//    ceil32(ctx_i + k_i) keys; the segments are laid end to end and a
-//    persistent grid, sized to the workgroups the GPU holds at once, gives
-//    every workgroup one equal contiguous share.  A workgroup walks the
+//    ceil32(ctx_i + k_i) keys; the segments are laid end to end, each
+//    after a lead-in of two blocks that stands for the cost of starting a
+//    piece on it, and a persistent grid, sized to the workgroups the GPU
+//    holds at once, gives every workgroup one equal contiguous share of
+//    that space (streaming plus piece starts).  A workgroup walks the
 //    segments its share touches; a segment it covers whole is written as
 //    bf16 directly, a segment cut at a share boundary leaves an fp32 partial
 //    (O, m, l) that the combine kernel merges in workgroup order.  Ragged
@@ -56,6 +58,11 @@ constexpr int kBlockKeys = 32;  // keys per inner step (two pages)
 // workgroup -- fewer cut segments, so less partial traffic and combine work,
 // and a longer pipeline per workgroup.
 constexpr int kMinShare = 8 * kBlockKeys;
+// Stream-K lead-in: every segment with keys counts kLeadKeys more in the
+// linear work space than it holds, the cost of starting a piece on it
+// (metadata, page ids, query rows, the ring's first blocks), so that equal
+// shares are equal in streaming plus piece starts.  A multiple of the block.
+constexpr int kLeadKeys = 2 * kBlockKeys;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8, v);
@@ -356,7 +363,8 @@ __device__ __forceinline__ void write_tile(const AttnParams &p, int g, bool comp
 // keys over the segments laid end to end (request-major, then KV head).
 struct Share {
   int start, end;
-  int i, g, off;  // segment and key offset where `start` falls
+  int i, g, off;  // segment and virtual offset where `start` falls
+  int lead;       // keys of lead-in per segment: kLeadKeys (stream-K) or 0
   ReqMeta first;  // request i's metadata, as read by the plan
 };
 
@@ -484,38 +492,56 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
       for (int i = lo; i < hi; ++i) npc += seg_pieces(segment_len(p, i), cap);
     }
   }
-  int total_pc;
-  const int excl_pc = block_excl_scan(npc, lds + kWaves, total_pc);
+  // Stream-K works in the virtual space where each segment with keys is
+  // lead keys longer (its lead-in first); the small-batch plan in keys.
+  const int lead = seg_mode ? 0 : kLeadKeys;
+  int total_pc = 0, total_v = total, excl_pc = 0, excl_v = excl, sum_v = sum;
+  if (seg_mode) {
+    excl_pc = block_excl_scan(npc, lds + kWaves, total_pc);
+  } else {
+    int nnz = 0;  // this thread's segments with keys
+    if (per == 1) {
+      nnz = sum > 0 ? 1 : 0;
+    } else {
+      for (int i = lo; i < hi; ++i) nnz += segment_len(p, i) > 0 ? 1 : 0;
+    }
+    sum_v = sum + lead * nnz;
+    excl_v = block_excl_scan(sum_v, lds + kWaves, total_v);
+    const int work_v = total_v * p.hkv;
+    share = (work_v + (int)gridDim.x - 1) / (int)gridDim.x;
+    share = max(kMinShare, round_up_block(share));
+  }
+  const int work_s = total_v * p.hkv;  // the plan's linear space (= work when seg_mode)
   if (blockIdx.x == 0) {
-    int acc = excl, acc_pc = excl_pc;
+    int acc = excl_v, acc_pc = excl_pc;
     for (int i = lo; i < hi; ++i) {
       const int seg = segment_len(p, i);
       p.plan[i] = acc;
       p.plan[B + 2 + i] = acc_pc;
-      acc += seg;
+      acc += seg > 0 ? seg + lead : 0;
       if (seg_mode) acc_pc += seg_pieces(seg, cap);
     }
     if (tid == 0) {
-      p.plan[B] = total;
+      p.plan[B] = total_v;
       p.plan[B + 1] = seg_mode ? -cap : share;  // negative: the small-batch cap
       p.plan[2 * B + 2] = total_pc;
     }
   }
   const int b = (int)blockIdx.x;
-  int start = work, end = work;
+  int start = work_s, end = work_s;
   if (!seg_mode) {
-    start = min(work, b * share);
-    end = min(work, start + share);
+    start = min(work_s, b * share);
+    end = min(work_s, start + share);
   }
   // the thread whose requests contain this workgroup's share locates it and
   // publishes the request's metadata, so the first piece needs no second
   // read of it
   const bool mine = seg_mode ? (b < total_pc * p.hkv && excl_pc * p.hkv <= b &&
                                 b < (excl_pc + npc) * p.hkv)
-                             : (start < work && excl * p.hkv <= start &&
-                                start < (excl + sum) * p.hkv);
+                             : (start < work_s && excl_v * p.hkv <= start &&
+                                start < (excl_v + sum_v) * p.hkv);
   if (mine) {
-    int acc = excl, acc_pc = excl_pc;
+    int acc = excl_v, acc_pc = excl_pc;
     for (int i = lo; i < hi; ++i) {
       if (per != 1) {
         q0 = p.cu[i];
@@ -523,6 +549,7 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
         cx = p.ctx[i];
       }
       const int seg = segment_of(p, q0, q1, cx);
+      const int segv = seg > 0 ? seg + lead : 0;  // seg when seg_mode
       const int n = seg_mode ? seg_pieces(seg, cap) : 0;
       int g = -1, off = 0, s0 = 0, s1 = 0;
       if (seg_mode) {
@@ -534,10 +561,10 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
           s0 = acc * p.hkv + g * seg + off;
           s1 = s0 + piece_begin(seg, n, q + 1) - off;
         }
-      } else if (start < (acc + seg) * p.hkv) {
+      } else if (start < (acc + segv) * p.hkv) {
         const int rel = start - acc * p.hkv;
-        g = rel / seg;
-        off = rel % seg;
+        g = rel / segv;
+        off = rel % segv;
         s0 = start;
         s1 = end;
       }
@@ -552,13 +579,14 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
         loc[7] = s1;
         break;
       }
-      acc += seg;
+      acc += segv;
       acc_pc += n;
     }
   }
   __syncthreads();
   Share sh;
-  const bool has = seg_mode ? b < total_pc * p.hkv : start < work;
+  sh.lead = lead;
+  const bool has = seg_mode ? b < total_pc * p.hkv : start < work_s;
   if (has) {
     sh.start = __builtin_amdgcn_readfirstlane(loc[6]);
     sh.end = __builtin_amdgcn_readfirstlane(loc[7]);
@@ -573,7 +601,7 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
     sh.first.len = sh.first.ctx + sh.first.k;
     sh.first.seg = segment_of(p, f0, f1, sh.first.ctx);
   } else {
-    sh.start = sh.end = work;
+    sh.start = sh.end = work_s;
     sh.i = sh.g = sh.off = 0;
     sh.first = ReqMeta{0, 0, 0, 0, 0};
   }
@@ -695,9 +723,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
       ++i;
       continue;
     }
-    const int take = min(rq.seg - off, sh.end - pos);
-    const int key_begin = off, key_end = min(rq.len, off + take);
-    const bool complete = off == 0 && take == rq.seg;
+    // offsets are virtual: the segment's keys follow its lead-in of
+    // sh.lead keys (none in the small-batch plan)
+    const int segv = rq.seg + sh.lead;
+    const int take = min(segv - off, sh.end - pos);
+    const int key_begin = max(off - sh.lead, 0);
+    const int key_end = min(rq.len, off + take - sh.lead);
+    if (key_end <= key_begin) break;  // the share ends inside the lead-in
+    const bool complete = off <= sh.lead && off + take == segv;
     const int slot = piece == 0 ? 0 : 1;
     c.kvw = reinterpret_cast<const char *>(p.kv) +
             (size_t)(kind * p.hkv + g) * kPage * D * sizeof(uint16_t);
@@ -771,7 +804,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
     pos += take;
     off += take;
     ++piece;
-    if (off == rq.seg) {
+    if (off == segv) {
       off = 0;
       if (++g == p.hkv) {
         g = 0;
@@ -832,7 +865,9 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
     b0 = pc_prefix * p.hkv + g * n;
     b1 = b0 + n - 1;
   } else {
-    b0 = start / share;
+    // stream-K: seg includes the lead-in, and the first workgroup with any
+    // of the segment's keys is the one holding the first key after it
+    b0 = (start + kLeadKeys) / share;
     b1 = (start + seg - 1) / share;
   }
   if (b0 == b1) return;  // one workgroup held the whole segment
