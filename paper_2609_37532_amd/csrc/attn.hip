@@ -14,7 +14,7 @@
 //    does not have (Eq. (2)'s padding applies per 16-row tile, not per 128).
 //  * Stream-K work split.  Each (request, KV head) pair is a segment of
 //    ceil32(ctx_i + k_i) keys; the segments are laid end to end, each
-//    after a lead-in of two blocks that stands for the cost of starting a
+//    after a lead-in of six blocks that stands for the cost of starting a
 //    piece on it, and a persistent grid, sized to the workgroups the GPU
 //    holds at once, gives every workgroup one equal contiguous share of
 //    that space (streaming plus piece starts).  A workgroup walks the
@@ -61,8 +61,9 @@ constexpr int kMinShare = 8 * kBlockKeys;
 // Stream-K lead-in: every segment with keys counts kLeadKeys more in the
 // linear work space than it holds, the cost of starting a piece on it
 // (metadata, page ids, query rows, the ring's first blocks), so that equal
-// shares are equal in streaming plus piece starts.  A multiple of the block.
-constexpr int kLeadKeys = 2 * kBlockKeys;
+// shares are equal in streaming plus piece starts.  A multiple of the block;
+// six blocks measured best across shapes (two to eight were compared).
+constexpr int kLeadKeys = 6 * kBlockKeys;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8, v);
