@@ -411,6 +411,12 @@ int dsv_read_probe(const void *buf, int32_t buf_tiles, const int32_t *order,
 #define DSV_TIMING_KINDS 8
 int dsv_timing_start(int32_t max_launches);
 int dsv_timing_stop(float *total_ms, int32_t *launches);
+/*
+ * Like dsv_timing_stop, but writes every recorded launch in order: ms[n] its
+ * duration in milliseconds and kinds[n] its kind, for at most `capacity`
+ * launches; *count receives the number written.  Turns timing off.
+ */
+int dsv_timing_stop_each(float *ms, int32_t *kinds, int32_t capacity, int32_t *count);
 
 /* Static text for a dsv_status value ("unknown status" otherwise). */
 const char *dsv_status_string(int status);

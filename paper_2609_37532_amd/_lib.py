@@ -78,6 +78,9 @@ def load():
         "dsv_timing_start": (ctypes.c_int, [I32]),
         "dsv_timing_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_float),
                                            ctypes.POINTER(ctypes.c_int32)]),
+        "dsv_timing_stop_each": (ctypes.c_int, [ctypes.POINTER(ctypes.c_float),
+                                                ctypes.POINTER(ctypes.c_int32), I32,
+                                                ctypes.POINTER(ctypes.c_int32)]),
         "dsv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     }
     for name, (res, args) in sig.items():
@@ -383,12 +386,29 @@ class KernelTimer:
         return self
 
     def __exit__(self, *exc):
-        ms = (ctypes.c_float * len(TIMING_KINDS))()
-        n = (ctypes.c_int32 * len(TIMING_KINDS))()
-        _check("dsv_timing_stop", load().dsv_timing_stop(ms, n))
-        self.result = {k: (float(ms[i]), int(n[i])) for i, k in enumerate(TIMING_KINDS)}
+        cap = self.max_launches
+        ms = (ctypes.c_float * cap)()
+        kinds = (ctypes.c_int32 * cap)()
+        count = ctypes.c_int32(0)
+        _check("dsv_timing_stop_each", load().dsv_timing_stop_each(ms, kinds, cap,
+                                                                   ctypes.byref(count)))
+        self.samples = {k: [] for k in TIMING_KINDS}
+        for n in range(count.value):
+            if 0 <= kinds[n] < len(TIMING_KINDS):
+                self.samples[TIMING_KINDS[kinds[n]]].append(float(ms[n]))
+        self.result = {k: (float(sum(v)), len(v)) for k, v in self.samples.items()}
         return False
 
     def mean_ms(self, kind: str) -> float:
         total, count = self.result[kind]
         return total / count if count else float("nan")
+
+    def median_ms(self, kind: str) -> float:
+        v = sorted(self.samples[kind])
+        if not v:
+            return float("nan")
+        h = len(v) // 2
+        return v[h] if len(v) % 2 else 0.5 * (v[h - 1] + v[h])
+
+    def count(self, kind: str) -> int:
+        return self.result[kind][1]

@@ -25,9 +25,12 @@ int check_dims(const dsv_attn_dims *d) {
   if ((long long)d->max_kv_len > (long long)d->max_pages_per_req * DSV_PAGE_SIZE)
     return DSV_ERR_DIMS;
   if (!(d->scale > 0.f) || !isfinite(d->scale)) return DSV_ERR_DIMS;
-  // the flattened work (KV heads x requests x keys) is indexed with int32
-  if ((long long)d->num_kv_heads * d->num_reqs * ((d->max_kv_len + 31) / 32 * 32) >= (1LL << 30))
-    return DSV_ERR_DIMS;
+  // the flattened work (KV heads x requests x keys, each segment after its
+  // stream-K lead-in) is indexed with int32
+  const long long seg_keys =
+      (long long)(d->max_kv_len + kAttnBlockKeys - 1) / kAttnBlockKeys * kAttnBlockKeys +
+      kAttnLeadKeys;
+  if ((long long)d->num_kv_heads * d->num_reqs * seg_keys >= (1LL << 30)) return DSV_ERR_DIMS;
   if (d->page_size != DSV_PAGE_SIZE) return DSV_ERR_UNSUPPORTED;
   if (d->head_dim != 64 && d->head_dim != 128) return DSV_ERR_UNSUPPORTED;
   if (!is_pow2_group(d->num_q_heads / d->num_kv_heads)) return DSV_ERR_UNSUPPORTED;

@@ -36,11 +36,14 @@
 //  * Transposed scores: S^T = K Q^T and O^T = V^T P^T with
 //    v_mfma_f32_16x16x32_bf16.  The score tile comes out with one query row
 //    per lane column, which is exactly the B-operand layout the PV product
-//    needs, so P never crosses lanes; the row max needs two row-swap
-//    permutes, and the row sum is one more MFMA against a tile of ones.
+//    needs, so P never crosses lanes; the row max and the row sum each need
+//    two row-swap permutes.  Each weight enters PV as a hi + lo pair of bf16
+//    values (two MFMAs per output tile), so the weights carry about 2^-17
+//    of their value and the output's own bf16 rounding dominates the error.
 //  * Lazy rescaling: the running maximum only moves (and the accumulators
 //    are only rescaled) when a block's maximum exceeds it by more than a
-//    factor 2^8, which keeps the weights below 2^8.
+//    factor 2^8, which keeps the weights below 2^8.  It is kept an integer,
+//    so rescales and merge weights are exact powers of two.
 //  * Waves of a workgroup split the dims when a request has one or two row
 //    tiles; with three or more row tiles each wave owns tiles.
 #include "dsv_internal.h"
@@ -52,7 +55,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kBlockKeys = 32;  // keys per inner step (two pages)
+constexpr int kBlockKeys = kAttnBlockKeys;  // keys per inner step (two pages)
 // Smallest stream-K share: with little work (short contexts, few requests)
 // eight blocks per workgroup beat spreading it over every resident
 // workgroup -- fewer cut segments, so less partial traffic and combine work,
@@ -63,7 +66,7 @@ constexpr int kMinShare = 8 * kBlockKeys;
 // (metadata, page ids, query rows, the ring's first blocks), so that equal
 // shares are equal in streaming plus piece starts.  A multiple of the block;
 // six blocks measured best across shapes (two to eight were compared).
-constexpr int kLeadKeys = 6 * kBlockKeys;
+constexpr int kLeadKeys = kAttnLeadKeys;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8, v);
@@ -129,7 +132,9 @@ struct Ring {
   static constexpr int kStage = 2 * kKRegion;          // 16 KiB at D = 128
   static constexpr int kKOps = 2 * kChunks;            // K operand tiles per block
 };
-constexpr int kStages = 3;      // ring stages = blocks in flight in registers
+// Ring stages = blocks in flight in registers.  Four (16 more VGPRs, 64 KiB
+// of ring) measured 1-3% slower than three at every shape.
+constexpr int kStages = 3;
 constexpr int kSubPages = 512;  // page ids staged in LDS at a time (8192 keys)
 
 // The wave's share of one block: one page's K or V tile (D/32 chunks of
@@ -209,19 +214,33 @@ __device__ __forceinline__ float row_max4(float x) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
+// Sum over the same four lanes.  Each swap hands every lane the pair in the
+// same order, so the four lanes end with bitwise equal sums.
+__device__ __forceinline__ float row_sum4(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // The running maximum is only raised when a block's maximum exceeds it by
 // more than this (base-2 units): weights then stay below 2^8, and the
 // accumulators are rescaled only on such a jump instead of every block.
+// The maximum is kept an integer (the block maximum rounded up), so every
+// rescale factor and every merge weight of the combine is an exact power of
+// two: where a segment is cut, or which rows share its tile, moves a row's
+// weights and sums by powers of two only, and its result changes only
+// through fp32 summation order.
 constexpr float kRescaleSlack = 8.f;
 
-// Online-softmax state of one lane: one query row (lane & 15); `lacc` holds
-// the row sum of the weights (every element, from an MFMA against ones);
+// Online-softmax state of one lane: one query row (lane & 15); `l` holds
+// the row sum of the weights (the same value in the row's four lanes);
 // for each of the wave's d blocks u (dims 16*(e_lo+u) + 4*(lane>>4) +
 // [0..3]), the 4 accumulated outputs.
 template <int D>
 struct RowState {
   float m;
-  f32x4 lacc;
+  float l;
   f32x4 o[D / 16];
 };
 
@@ -277,27 +296,39 @@ __device__ __forceinline__ void ring_compute(const char *ring, uint32_t so, cons
                      fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
   bmax = row_max4(bmax) * scale_log2;
   if (__builtin_amdgcn_ballot_w64(bmax > st.m + kRescaleSlack) != 0) {
-    const float m_new = fmaxf(st.m, bmax);
+    const float m_new = fmaxf(st.m, ceilf(bmax));
     // 0 on a row's first visible block, 1 for a row that still sees nothing
     const float alpha = __builtin_amdgcn_exp2f(st.m - (m_new == -INFINITY ? 0.f : m_new));
-    st.lacc *= alpha;
+    st.l *= alpha;
 #pragma unroll
     for (int u = 0; u < NE; ++u) st.o[u] *= alpha;
     st.m = m_new;
   }
   const float neg_m = st.m == -INFINITY ? 0.f : -st.m;
-  // P in bf16 (the PV operand); the row sum uses the same rounded weights
-  uint32_t pk[4];
+  // P enters the bf16 PV product as a pair: hi = P rounded to bf16 and
+  // lo = the remainder rounded to bf16, so hi + lo carries P to about 2^-17
+  // of its value and the weights add no error next to the output's own bf16
+  // rounding.  The row sum adds the fp32 weights themselves: the lane's
+  // eight, then across the row's four lanes.
+  uint32_t pk[4], pl[4];
+  float psum = 0.f;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][0], scale_log2, neg_m));
-    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][1], scale_log2, neg_m));
-    const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][2], scale_log2, neg_m));
-    const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][3], scale_log2, neg_m));
-    pk[2 * h] = pack_bf16x2(p0, p1);
-    pk[2 * h + 1] = pack_bf16x2(p2, p3);
+    float pw[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      pw[q] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[h][q], scale_log2, neg_m));
+    psum += (pw[0] + pw[1]) + (pw[2] + pw[3]);
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+      const uint32_t hi = pack_bf16x2(pw[2 * w], pw[2 * w + 1]);
+      pk[2 * h + w] = hi;
+      pl[2 * h + w] = pack_bf16x2(pw[2 * w] - __uint_as_float(hi << 16),
+                                  pw[2 * w + 1] - __uint_as_float(hi & 0xFFFF0000u));
+    }
   }
   const bf16x8 pb = as_bf16x8(make_uint4(pk[0], pk[1], pk[2], pk[3]));
+  const bf16x8 pbl = as_bf16x8(make_uint4(pl[0], pl[1], pl[2], pl[3]));
   // V element q of this lane is key t0 + 8kq + q.  Keys at or past key_end
   // may hold anything (even NaN): zero their V so that 0 * V stays 0.
   if (!full) {
@@ -315,11 +346,13 @@ __device__ __forceinline__ void ring_compute(const char *ring, uint32_t so, cons
       vop[u].w &= vmask[3];
     }
   }
-  const uint4 ones = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
-  st.lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ones), pb, st.lacc, 0, 0, 0);
 #pragma unroll
   for (int u = 0; u < NE; ++u)
     st.o[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vop[u]), pb, st.o[u], 0, 0, 0);
+#pragma unroll
+  for (int u = 0; u < NE; ++u)
+    st.o[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vop[u]), pbl, st.o[u], 0, 0, 0);
+  st.l += row_sum4(psum);
 }
 
 // Writes a finished row tile for the wave's `ne` d blocks from e_lo: bf16
@@ -656,32 +689,48 @@ __device__ __forceinline__ void ring_step(const RingCtx<D> &c, char *ring, int b
   }
 }
 
+// Steps S .. kStages-1 of one round of the block loop (one step per ring
+// stage, the stage index a compile-time constant); true once the sub-piece's
+// last block has been computed.
+template <int D, int NE, int S>
+struct RingRound {
+  static __device__ __forceinline__ bool run(const RingCtx<D> &c, char *ring, int b,
+                                             StageRegs<D> (&r)[kStages],
+                                             const bf16x8 (&qv)[D / 32], float scale_log2,
+                                             int lane, RowState<D> &st) {
+    ring_step<D, NE, S>(c, ring, b + S, r[S], qv, scale_log2, lane, st);
+    if (b + S + 1 >= c.nblk) return true;
+    return RingRound<D, NE, S + 1>::run(c, ring, b, r, qv, scale_log2, lane, st);
+  }
+};
+template <int D, int NE>
+struct RingRound<D, NE, kStages> {
+  static __device__ __forceinline__ bool run(const RingCtx<D> &, char *, int,
+                                             StageRegs<D> (&)[kStages],
+                                             const bf16x8 (&)[D / 32], float, int,
+                                             RowState<D> &) {
+    return false;
+  }
+};
+
 // All blocks of one sub-piece through the ring.
 template <int D, int NE>
 __device__ __forceinline__ void ring_run(const RingCtx<D> &c, char *ring,
                                          const bf16x8 (&qv)[D / 32], float scale_log2, int lane,
                                          RowState<D> &st) {
-  static_assert(kStages == 3, "the block loop below is unrolled for three stages");
   // issued in block order (the empty asm keeps the compiler from reordering
   // them), so that each step waits only for its own block
-  StageRegs<D> r0, r1, r2;
-  stage_load<D>(tile_of<D>(c, 0), c.voff, r0);
-  asm volatile("" ::: "memory");
-  stage_load<D>(tile_of<D>(c, 1), c.voff, r1);
-  asm volatile("" ::: "memory");
-  stage_load<D>(tile_of<D>(c, 2), c.voff, r2);
-  asm volatile("" ::: "memory");
-  // the loop leaves only through the breaks, so every path back to its head
-  // has issued the same loads in the same order and the compiler can wait
-  // for exactly the block each step writes
-  for (int b = 0;; b += kStages) {
-    ring_step<D, NE, 0>(c, ring, b, r0, qv, scale_log2, lane, st);
-    if (b + 1 >= c.nblk) break;
-    ring_step<D, NE, 1>(c, ring, b + 1, r1, qv, scale_log2, lane, st);
-    if (b + 2 >= c.nblk) break;
-    ring_step<D, NE, 2>(c, ring, b + 2, r2, qv, scale_log2, lane, st);
-    if (b + 3 >= c.nblk) break;
+  StageRegs<D> r[kStages];
+#pragma unroll
+  for (int s = 0; s < kStages; ++s) {
+    stage_load<D>(tile_of<D>(c, s), c.voff, r[s]);
+    asm volatile("" ::: "memory");
   }
+  // the loop leaves only when a round reports the last block, so every path
+  // back to its head has issued the same loads in the same order and the
+  // compiler can wait for exactly the block each step writes
+  for (int b = 0;; b += kStages)
+    if (RingRound<D, NE, 0>::run(c, ring, b, r, qv, scale_log2, lane, st)) break;
   __syncthreads();  // the ring is free for the next sub-piece
 }
 
@@ -771,7 +820,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
       }
       RowState<D> st;
       st.m = -INFINITY;
-      st.lacc = f32x4{0.f, 0.f, 0.f, 0.f};
+      st.l = 0.f;
 #pragma unroll
       for (int e = 0; e < D / 16; ++e) st.o[e] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -799,7 +848,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
         else
           ring_run<D, D / 64>(c, ring, qv, p.scale_log2, lane, st);
       }
-      if (c.active) write_tile<D>(p, g, complete, slot, rq, rt, e_lo, ne, lane, st.lacc[0], st);
+      if (c.active) write_tile<D>(p, g, complete, slot, rq, rt, e_lo, ne, lane, st.l, st);
     }
 
     pos += take;

@@ -19,6 +19,13 @@ constexpr int kWave = 64;
 constexpr int kPage = DSV_PAGE_SIZE;  // tokens per KV page
 constexpr int kMaxQlen = DSV_MAX_QLEN;
 
+// Verify attention: keys per inner step of the stream-K kernel (two pages),
+// and the lead-in of virtual keys that its plan puts in front of every
+// segment with keys (the cost of starting a piece on it, six blocks).  The
+// host's int32 guard on the flattened work counts the lead-in too.
+constexpr int kAttnBlockKeys = 32;
+constexpr int kAttnLeadKeys = 6 * kAttnBlockKeys;
+
 // -------------------------------------------------------------------------
 // verify attention
 // -------------------------------------------------------------------------

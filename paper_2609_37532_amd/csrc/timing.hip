@@ -106,4 +106,25 @@ int dsv_timing_stop(float *total_ms, int32_t *launches) {
   return rc;
 }
 
+int dsv_timing_stop_each(float *ms, int32_t *kinds, int32_t capacity, int32_t *count) {
+  if (!ms || !kinds || !count) return DSV_ERR_NULL;
+  if (capacity < 0) return DSV_ERR_DIMS;
+  Timing &t = timing();
+  int rc = DSV_OK, n_out = 0;
+  for (int n = 0; n < t.used && n_out < capacity; ++n) {
+    float v = 0.f;
+    if (hipEventSynchronize(t.stop[n]) != hipSuccess ||
+        hipEventElapsedTime(&v, t.start[n], t.stop[n]) != hipSuccess) {
+      rc = DSV_ERR_HIP;
+      continue;
+    }
+    ms[n_out] = v;
+    kinds[n_out] = t.kind[n];
+    ++n_out;
+  }
+  *count = n_out;
+  release(t);
+  return rc;
+}
+
 }  // extern "C"

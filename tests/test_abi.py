@@ -106,6 +106,29 @@ def test_workspace_is_bounded_by_the_grid_not_the_context():
     assert ws(num_reqs=65535, max_kv_len=8192) == 0
 
 
+def test_int32_guard_counts_the_stream_k_lead_in():
+    # The plan lays every segment after a lead-in of 192 virtual keys.  Here
+    # the keys alone fit int32 indexing (256 * 65535 * 32 = 5.4e8 < 2^30),
+    # but with the lead-in the work space is 256 * 65535 * 224 = 3.8e9 and
+    # would overflow: the shape is refused before anything is enqueued.
+    lib = dsv.load()
+    d = good_dims(num_reqs=65535, num_kv_heads=256, num_q_heads=256, max_kv_len=32,
+                  max_pages_per_req=2)
+    assert lib.dsv_verify_attn_workspace_bytes(ctypes.byref(d)) == 0
+    fake = 1 << 20
+    assert lib.dsv_verify_attn(fake, fake, fake, fake, fake, fake, ctypes.byref(d), fake,
+                               1 << 30, None) == -2
+    # the boundary: the largest B that still fits with the lead-in is accepted
+    seg = 32 + 192
+    b_max = ((1 << 30) - 1) // (256 * seg)
+    ok = good_dims(num_reqs=b_max, num_kv_heads=256, num_q_heads=256, max_kv_len=32,
+                   max_pages_per_req=2)
+    assert lib.dsv_verify_attn_workspace_bytes(ctypes.byref(ok)) > 0
+    over = good_dims(num_reqs=b_max + 1, num_kv_heads=256, num_q_heads=256, max_kv_len=32,
+                     max_pages_per_req=2)
+    assert lib.dsv_verify_attn_workspace_bytes(ctypes.byref(over)) == 0
+
+
 def test_accept_rejects_bad_arguments():
     lib = dsv.load()
     fake = 1 << 20

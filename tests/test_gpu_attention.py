@@ -1,11 +1,14 @@
 """GPU parity of dsv_verify_attn against the fp64 oracle (through the C ABI).
 
 Bar: max-abs error <= 1e-2 (or, where the bf16 output cannot hold that,
-2^-8 |oracle| + 2e-3) and mean-abs error <= 1e-3 over live rows, tail
-rows exactly zero, every output finite although every element the kernel
-must not read is NaN (tail q rows, dead slots of last pages, spare pages).
+the bf16 half-spacing at |oracle| + 2e-3, which only happens from
+|oracle| = 4 up) and mean-abs error <= 1e-3 over live rows, tail rows
+exactly zero, every output finite although every element the kernel must
+not read is NaN (tail q rows, dead slots of last pages, spare pages).
 Invariants that the design makes exact are checked bitwise (page
-permutation, run-to-run determinism); packing independence within tolerance.
+permutation, run-to-run determinism); packing independence and prefix
+stability within one bf16 spacing of the first run's value (plus an fp32
+slack of 2^-12).
 """
 import zlib
 
@@ -18,7 +21,7 @@ import workloads as W
 pytestmark = pytest.mark.gpu
 
 try:
-    from gpu_util import AttnDev, assert_attn_close, run_attn, say
+    from gpu_util import AttnDev, assert_attn_close, assert_same_up_to_rounding, run_attn, say
 except Exception:  # pragma: no cover
     pass
 
@@ -143,7 +146,12 @@ def test_long_context():
 
 
 def test_peaked_scores():
-    # Q scaled by 4 makes the softmax peaky; bf16-aware bound.
+    # Q scaled by 4 makes the softmax peaky: few keys carry the weight, so
+    # the bf16 rounding of the weights averages out less.  Every element is
+    # still held to the per-element bound (1e-2 below |x| = 4); the mean is
+    # reported, not bounded, since it is no longer an average over many
+    # small independent errors.
+    from gpu_util import attn_bound
     inp = case(91, [800, 50, 2000, 9], [16, 3, 6, 1], q_scale=4.0)
     say("attn", "peaked")
     got = run_attn(inp)
@@ -151,7 +159,8 @@ def test_peaked_scores():
     live = int(inp.cu_qlens[-1])
     assert np.isfinite(got).all()
     err = np.abs(got[:live] - ref[:live])
-    assert (err <= 1e-2 + 2.0 ** -8 * np.abs(ref[:live])).all(), float(err.max())
+    say("attn", "peaked: max %.3g mean %.3g" % (err.max(), err.mean()))
+    assert (err <= attn_bound(ref[:live])).all(), float(err.max())
 
 
 def test_closed_form_single_key_is_exact():
@@ -167,9 +176,10 @@ def test_closed_form_single_key_is_exact():
 # ------------------------------------------------------------ exact invariants
 def test_packing_independence():
     # The same requests packed in another order, with sentinels and another
-    # capacity, give the same rows (within the tolerance: the stream-K share
-    # boundaries depend on the batch's total work, so the fp32 merge order of
-    # a request can change with the packing).
+    # capacity, give the same rows up to rounding: the stream-K share
+    # boundaries depend on the batch's total work, so another packing can
+    # cut a request's segments elsewhere, which changes its fp32 summation
+    # order (weights only move by powers of two).
     inp = W.config_attn_inputs(3)
     say("attn", "packing independence")
     base = run_attn(inp)
@@ -180,9 +190,11 @@ def test_packing_independence():
         gaps = list(rng.integers(0, 2, size=B + 1))
         alt = W.repack(inp, order, capacity=int(inp.qlens.sum()) + 17, gaps=gaps)
         got = run_attn(alt)
+        worst = 0.0
         for old_i, new_i, o_old, o_new, k in alt.meta["moves"]:
-            d = np.abs(got[o_new:o_new + k] - base[o_old:o_old + k])
-            assert d.max() <= 2.0 ** -7, (old_i, d.max())
+            worst = max(worst, assert_same_up_to_rounding(
+                got[o_new:o_new + k], base[o_old:o_old + k], "request %d" % old_i))
+        say("attn", "packing trial %d: max diff %.3g" % (trial, worst))
         assert not got[int(alt.cu_qlens[-1]):].any()
 
 
@@ -213,9 +225,10 @@ def test_determinism_bitwise():
     assert np.array_equal(d.result(), first)
 
 
-def test_prefix_stability_within_tolerance():
-    # Row j does not depend on k_i while j < k_i (up to rounding: the work
-    # split changes with the number of live rows).
+def test_prefix_stability_up_to_rounding():
+    # Row j does not depend on k_i while j < k_i, up to rounding: the work
+    # split and the rows that share a tile change with the number of live
+    # rows.
     base = case(31, [1500], [16], cap=16)
     say("attn", "prefix stability")
     full = run_attn(base)
@@ -227,7 +240,8 @@ def test_prefix_stability_within_tolerance():
                            page_size=base.page_size, max_kv_len=base.max_kv_len,
                            scale=base.scale)
         got = run_attn(alt)
-        assert np.abs(got[:k] - full[:k]).max() <= 2.0 ** -7
+        d = assert_same_up_to_rounding(got[:k], full[:k], "k=%d" % k)
+        say("attn", "prefix stability k=%d: max diff %.3g" % (k, d))
 
 
 # ------------------------------------------------------------ random sweep

@@ -39,6 +39,43 @@ def test_hand_example():
         assert lo <= us < hi
 
 
+def test_successor_interval_exact():
+    # Two rows with different logits, so a wrong row index shows.  Row 0:
+    # P = [1/6, 2/6, 3/6]; row 1: P = [4/10, 1/10, 5/10] (T = 1).  Each
+    # token's interval [lo, hi) in the successor distribution is the
+    # cumulative probability of the tokens before it, renormalised after the
+    # rejected candidate is removed.
+    L = np.log(np.array([[1, 2, 3], [4, 1, 5]], np.float64)).astype(np.float32)
+    sixth, tenth = 1.0 / 6.0, 0.1
+    want = {
+        (0, -1): [(0, sixth), (sixth, 0.5), (0.5, 1.0)],
+        (0, 2): [(0, 1 / 3), (1 / 3, 1.0), (1.0, 1.0)],        # x = 2 rejected
+        (0, 0): [(0, 0), (0, 0.4), (0.4, 1.0)],                # x = 0 rejected
+        (0, 1): [(0, 0.25), (0.25, 0.25), (0.25, 1.0)],        # x = 1 rejected
+        (1, -1): [(0, 0.4), (0.4, 0.5), (0.5, 1.0)],
+        (1, 2): [(0, 0.8), (0.8, 1.0), (1.0, 1.0)],
+        (1, 0): [(0, 0), (0, 1 / 6), (1 / 6, 1.0)],
+        (1, 7): [(0, 0.4), (0.4, 0.5), (0.5, 1.0)],            # out-of-vocabulary id
+    }
+    for (row, removed), ivs in want.items():
+        for tok, (lo_w, hi_w) in enumerate(ivs):
+            lo, hi = oracle.successor_interval(L, "f32", row, removed, 1.0, tok)
+            assert abs(lo - lo_w) < 1e-6 and abs(hi - hi_w) < 1e-6, (row, removed, tok, lo, hi)
+    # temperature divides the logits: T = 2 gives P proportional to sqrt([1, 2, 3])
+    r = np.sqrt([1.0, 2.0, 3.0])
+    r /= r.sum()
+    lo, hi = oracle.successor_interval(L, "f32", 0, -1, 2.0, 1)
+    assert abs(lo - r[0]) < 1e-6 and abs(hi - r[0] - r[1]) < 1e-6
+    # with x = 0 removed at T = 2
+    lo, hi = oracle.successor_interval(L, "f32", 0, 0, 2.0, 2)
+    assert abs(lo - r[1] / (1 - r[0])) < 1e-6 and abs(hi - 1.0) < 1e-6
+    for bad in [dict(temperature=0.0), dict(token=3), dict(token=-1)]:
+        kw = dict(temperature=1.0, token=0)
+        kw.update(bad)
+        with pytest.raises(ValueError):
+            oracle.successor_interval(L, "f32", 0, -1, kw["temperature"], kw["token"])
+
+
 def batch(rng, n, rows_logits, draft_block, T, dtype="f32"):
     """n identical requests of k = len(rows_logits) rows with fresh uniforms."""
     k, V = rows_logits.shape
