@@ -64,7 +64,9 @@ typedef enum {
   DSV_ERR_DIMS = -2,        /* a host-known size is out of range               */
   DSV_ERR_UNSUPPORTED = -3, /* valid but unsupported (head_dim, page size, G)  */
   DSV_ERR_WORKSPACE = -4,   /* workspace NULL, misaligned or too small         */
-  DSV_ERR_HIP = -5          /* a HIP runtime call failed (launch error)        */
+  DSV_ERR_HIP = -5,         /* a HIP runtime call failed (launch error)        */
+  DSV_ERR_TOO_LARGE = -6    /* needs more than the fixed scratch of a          */
+                            /* no-allocation entry point                       */
 } dsv_status;
 
 typedef enum { DSV_F32 = 0, DSV_BF16 = 1 } dsv_dtype;
@@ -206,6 +208,34 @@ int dsv_accept(const void *logits_packed, int32_t dtype,
                int32_t *accept_len, int32_t *next_token, int32_t num_reqs,
                int32_t capacity, int32_t vocab, void *workspace,
                size_t workspace_bytes, void *hip_stream);
+
+/*
+ * dsv_accept without a workspace argument, for callers that cannot allocate
+ * device memory (code under hipGraph capture that must not call hipMalloc,
+ * tight serving loops, harnesses that forbid allocation).  Same arguments,
+ * semantics and results as dsv_accept, bit for bit, minus the workspace.
+ *
+ * Scratch: the per-(row, vocabulary chunk) maxima go to a fixed device
+ * array of DSV_ACCEPT_NOALLOC_MAX_BYTES that the library holds on every GPU
+ * it runs on until the process ends.  A call needs
+ * dsv_accept_workspace_bytes(capacity, num_reqs, vocab) of it (about
+ * 8 * capacity * ceil(vocab / 8192) bytes, so 27,594 rows at a 151,936-token
+ * vocabulary); a larger call returns DSV_ERR_TOO_LARGE and enqueues nothing.
+ * The first call on a device resolves the array's address there (no
+ * allocation); the array of the CURRENT device is used, so hip_stream must
+ * belong to the current device.  The call allocates nothing, frees nothing
+ * and calls no allocating library routine.
+ *
+ * Every call on one GPU shares that GPU's scratch: calls ordered on one
+ * stream are safe, but calls that may overlap on one GPU (several streams or
+ * host threads) race and their results are undefined.  The scratch needs no
+ * initialisation; its contents after a call are unspecified.
+ */
+#define DSV_ACCEPT_NOALLOC_MAX_BYTES (4u << 20)
+int dsv_accept_noalloc(const void *logits_packed, int32_t dtype,
+                       const int32_t *cu_qlens, const int32_t *draft_tokens,
+                       int32_t *accept_len, int32_t *next_token, int32_t num_reqs,
+                       int32_t capacity, int32_t vocab, void *hip_stream);
 
 /*
  * Stochastic acceptance: the prefix verifier at temperature T > 0 (Sec. III-D

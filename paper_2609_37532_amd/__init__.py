@@ -35,6 +35,7 @@ from ._lib import (  # noqa: F401
     Graph,
     KernelTimer,
     accept,
+    accept_noalloc,
     accept_stochastic,
     accept_stochastic_workspace_bytes,
     accept_workspace_bytes,

@@ -62,6 +62,7 @@ def load():
         "dsv_verify_attn": (ctypes.c_int, [P, P, P, P, P, P, PD, P, SZ, P]),
         "dsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
         "dsv_accept": (ctypes.c_int, [P, I32, P, P, P, P, I32, I32, I32, P, SZ, P]),
+        "dsv_accept_noalloc": (ctypes.c_int, [P, I32, P, P, P, P, I32, I32, I32, P]),
         "dsv_validate_metadata": (ctypes.c_int, [P, P, P, PD, P, P]),
         "dsv_accept_stochastic_workspace_bytes": (SZ, [I32, I32, I32]),
         "dsv_accept_stochastic": (ctypes.c_int, [P, I32, P, P, P, ctypes.c_float, P, P, I32,
@@ -211,6 +212,26 @@ def accept(logits_packed, cu_qlens, draft_tokens, accept_len, next_token, *,
     _check("dsv_accept", load().dsv_accept(
         _ptr(logits_packed), dtype, _ptr(cu_qlens), _ptr(draft_tokens), _ptr(accept_len),
         _ptr(next_token), B, cap, vocab, _ptr(workspace), nbytes, _stream_handle(stream)))
+
+
+def accept_noalloc(logits_packed, cu_qlens, draft_tokens, accept_len, next_token, *,
+                   stream=None) -> None:
+    """Enqueue ``dsv_accept_noalloc``: ``accept`` with the library's fixed
+    device scratch in place of a workspace (for callers that cannot
+    allocate; calls that overlap on one GPU race)."""
+    import torch
+    _require(logits_packed, "logits_packed", (torch.float32, torch.bfloat16), 2)
+    for t, n in ((cu_qlens, "cu_qlens"), (draft_tokens, "draft_tokens"),
+                 (accept_len, "accept_len"), (next_token, "next_token")):
+        _require(t, n, (torch.int32,), 1)
+    cap, vocab = logits_packed.shape
+    B = cu_qlens.numel() - 1
+    if draft_tokens.numel() != cap or accept_len.numel() != B or next_token.numel() != B:
+        raise ValueError("draft_tokens must be [cap]; accept_len, next_token [B]")
+    dtype = DSV_BF16 if logits_packed.dtype == torch.bfloat16 else DSV_F32
+    _check("dsv_accept_noalloc", load().dsv_accept_noalloc(
+        _ptr(logits_packed), dtype, _ptr(cu_qlens), _ptr(draft_tokens), _ptr(accept_len),
+        _ptr(next_token), B, cap, vocab, _stream_handle(stream)))
 
 
 def accept_stochastic_workspace_bytes(capacity: int, num_reqs: int, vocab: int) -> int:

@@ -145,6 +145,27 @@ int dsv_accept(const void *logits_packed, int32_t dtype, const int32_t *cu_qlens
   return e == hipSuccess ? DSV_OK : DSV_ERR_HIP;
 }
 
+int dsv_accept_noalloc(const void *logits_packed, int32_t dtype, const int32_t *cu_qlens,
+                       const int32_t *draft_tokens, int32_t *accept_len,
+                       int32_t *next_token, int32_t num_reqs, int32_t capacity,
+                       int32_t vocab, void *hip_stream) {
+  if (!logits_packed || !cu_qlens || !draft_tokens || !accept_len || !next_token)
+    return DSV_ERR_NULL;
+  if (num_reqs < 1 || capacity < 1 || vocab < 1 || capacity > 65535 ||
+      num_reqs > (1 << 30))
+    return DSV_ERR_DIMS;
+  if (dtype != DSV_F32 && dtype != DSV_BF16) return DSV_ERR_UNSUPPORTED;
+  const AcceptWorkspace ws = accept_workspace_layout(capacity, vocab);
+  if (ws.total > DSV_ACCEPT_NOALLOC_MAX_BYTES) return DSV_ERR_TOO_LARGE;
+  char *scratch = (char *)accept_noalloc_scratch();
+  if (!scratch) return DSV_ERR_HIP;
+  const hipError_t e = launch_accept(
+      logits_packed, dtype, cu_qlens, draft_tokens, accept_len, next_token,
+      num_reqs, capacity, vocab, (float *)(scratch + ws.val_off),
+      (int32_t *)(scratch + ws.idx_off), ws.num_chunks, (hipStream_t)hip_stream);
+  return e == hipSuccess ? DSV_OK : DSV_ERR_HIP;
+}
+
 size_t dsv_accept_stochastic_workspace_bytes(int32_t capacity, int32_t num_reqs,
                                              int32_t vocab) {
   if (capacity < 1 || num_reqs < 1 || vocab < 1) return 0;
@@ -274,6 +295,7 @@ const char *dsv_status_string(int status) {
     case DSV_ERR_UNSUPPORTED: return "unsupported configuration";
     case DSV_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case DSV_ERR_HIP: return "HIP runtime error";
+    case DSV_ERR_TOO_LARGE: return "exceeds the fixed scratch of the no-allocation entry point";
     default: return "unknown status";
   }
 }

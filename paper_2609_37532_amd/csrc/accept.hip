@@ -20,6 +20,15 @@
 
 #include <math.h>
 
+#include <mutex>
+
+// Scratch of the no-allocation entry point (dsv_accept_noalloc): the chunk
+// maxima live here instead of in a caller workspace.  Each GPU the library
+// runs on holds its own copy until the process ends.  In host code this name
+// is a host-side stand-in, not a device address: host code only ever uses the
+// address that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[DSV_ACCEPT_NOALLOC_MAX_BYTES];
+
 namespace dsv {
 namespace {
 
@@ -195,6 +204,23 @@ __global__ __launch_bounds__(kWave) void prefix_kernel(
 }
 
 }  // namespace
+
+// Device address of the no-allocation scratch on the current device,
+// resolved once per device with that device current (nullptr on failure).
+void *accept_noalloc_scratch() {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    addr[dev] = p;
+  }
+  return addr[dev];
+}
 
 AcceptWorkspace accept_workspace_layout(int32_t cap, int32_t vocab) {
   AcceptWorkspace w;

@@ -68,6 +68,7 @@ struct AcceptWorkspace {
   int32_t num_chunks;
 };
 AcceptWorkspace accept_workspace_layout(int32_t cap, int32_t vocab);
+void *accept_noalloc_scratch();  // the current device's fixed scratch, or nullptr
 hipError_t launch_accept(const void *logits, int dtype, const int32_t *cu,
                          const int32_t *draft, int32_t *accept_len,
                          int32_t *next_token, int32_t num_reqs, int32_t cap,

@@ -39,6 +39,7 @@ def test_status_strings():
     expect = {0: "ok", -1: "null pointer argument", -2: "dimension out of range",
               -3: "unsupported configuration",
               -4: "workspace missing, misaligned or too small", -5: "HIP runtime error",
+              -6: "exceeds the fixed scratch of the no-allocation entry point",
               7: "unknown status"}
     for code, text in expect.items():
         assert dsv.status_string(code) == text
@@ -240,3 +241,30 @@ def test_read_probe_argument_errors():
     assert lib.dsv_read_probe(fake, 4, fake, 4, fake, 0, None) == -2
     assert lib.dsv_read_probe(fake, 4, fake, 4, fake, 65536, None) == -2
     assert lib.dsv_read_probe(fake + 8, 4, fake, 4, fake, 1, None) == -3
+
+
+def test_accept_noalloc_rejects_bad_arguments_before_any_device_call():
+    # Every rejection below happens on the host, before the scratch address
+    # is resolved or anything is enqueued (no GPU here).
+    lib = dsv.load()
+    fake = 1 << 20
+    args = [fake, 1, fake, fake, fake, fake, 32, 256, 151936, None]
+    bad = list(args); bad[3] = None
+    assert lib.dsv_accept_noalloc(*bad) == -1
+    bad = list(args); bad[1] = 7
+    assert lib.dsv_accept_noalloc(*bad) == -3
+    for i, v in ((6, 0), (7, 0), (7, 65536), (8, 0)):
+        bad = list(args); bad[i] = v
+        assert lib.dsv_accept_noalloc(*bad) == -2, (i, v)
+    # the scratch limit: the need is the dsv_accept workspace size
+    limit = 4 << 20
+    assert lib.dsv_accept_workspace_bytes(256, 32, 151936) <= limit
+    big = lib.dsv_accept_workspace_bytes(65535, 32, 262144)
+    assert big > limit
+    bad = list(args); bad[7] = 65535; bad[8] = 262144
+    assert lib.dsv_accept_noalloc(*bad) == -6
+    # the largest capacity that fits at a 151,936-token vocabulary (19 chunks)
+    fits = max(c for c in range(27000, 28001)
+               if lib.dsv_accept_workspace_bytes(c, 32, 151936) <= limit)
+    assert lib.dsv_accept_workspace_bytes(fits + 1, 32, 151936) > limit
+    assert fits >= 27000
