@@ -130,6 +130,29 @@ def cpu_threads():
     return max(1, min(n, os.cpu_count() or 1))
 
 
+def cpu_model():
+    """The host CPU's model name (lscpu, else /proc/cpuinfo) and its logical CPUs."""
+    import subprocess
+    name = None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.strip().startswith("Model name:"):
+                name = line.split(":", 1)[1].strip()
+                break
+    except Exception:
+        pass
+    if name is None:
+        try:
+            for line in open("/proc/cpuinfo"):
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+        except Exception:
+            name = "unknown"
+    return {"model": name, "logical_cpus": os.cpu_count()}
+
+
 def cpu_baseline(attn, acc, seconds):
     """fp64 oracle over the requests of the same batch (attention rows of a
     request + its acceptance rows), repeating passes over the batch for about
@@ -165,7 +188,9 @@ def cpu_baseline(attn, acc, seconds):
             if t_total >= seconds:
                 break
         passes += 1
+    host = cpu_model()
     single = {"value": done_tokens / t_total, "unit": UNIT, "cores": 1, "kind": "oracle",
+              "cpu": host,
               "sample": "%d request-verifications (%d passes over the %d live requests of "
                         "the same batch, %d packed rows): fp64 attention over each "
                         "request's keys + acceptance of its rows, %.1f s, single thread"
@@ -179,6 +204,7 @@ def cpu_baseline(attn, acc, seconds):
             mt_passes += 1
         wall = time.perf_counter() - t0
     multi = {"value": mt_tokens / wall, "unit": UNIT, "cores": threads, "kind": "oracle",
+             "cpu": host,
              "sample": "%d whole passes over the %d live requests of the same batch (%d "
                        "packed rows): fp64 attention + acceptance per request, requests "
                        "spread over %d host threads, %.1f s wall"
@@ -202,7 +228,7 @@ def stress_bench(steps):
     st = plan.draw_step()
     run.stage(st)
     run.capture()
-    times, tokens, kv_bytes, exact = [], 0, 0, True
+    times, tokens, kv_bytes, step_other, exact = [], 0, 0, 0, True
     hq, hkv, d = run.hq, run.hkv, run.d
     for step in range(steps):
         if step > 0:
@@ -210,6 +236,8 @@ def stress_bench(steps):
             run.stage(st)
         keys = (run.ctx_host + st.qlens)[st.qlens > 0]
         kv_bytes += int(keys.sum()) * hkv * d * 2 * 2 * plan.num_layers
+        live = int(st.qlens.sum())
+        step_other += live * hq * d * 2 * 2 * plan.num_layers + live * plan.vocab * 2
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(run.stream)
@@ -228,10 +256,13 @@ def stress_bench(steps):
             "us_per_layer_incl_accept": round(total_ms / steps * 1e3 / plan.num_layers, 2),
             "packed_tokens_per_s": round(tokens / (total_ms * 1e-3), 1),
             "kv_gbps": round(kv_bytes / (total_ms * 1e-3) / 1e9, 1),
+            "kv_frac": round(kv_bytes / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "step_frac": round((kv_bytes + step_other) / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "step_frac_counts": "KV of every layer + q/out rows + logits of live rows",
             "acceptance_exact_every_step": exact}
 
 
-def configs_bench(reps=50):
+def configs_bench(reps=200):
     """Verify attention alone on the other attention presets (configs 2 and
     3: Qwen3-4B shape B=8 with full blocks over contexts U[256, 2048], and
     Qwen3-8B shape B=16 packed over U[512, 4096]) and config 4 for
@@ -268,16 +299,23 @@ def configs_bench(reps=50):
                     scrub.fill_(r & 0xFF)
                 run()
             torch.cuda.synchronize()
-        t_split = tm.mean_ms("attn_split") * 1e-3
-        t_comb = tm.mean_ms("attn_combine") * 1e-3
+        t_split = tm.median_ms("attn_split") * 1e-3
+        t_comb = tm.median_ms("attn_combine") * 1e-3
         nbytes = attention_bytes(attn, attn.num_kv_heads, attn.num_q_heads, attn.head_dim)
         toks = int(attn.qlens.sum())
+        t_op = t_split + t_comb
         out["config_%d" % idx] = {
             "B": attn.num_reqs, "packed_tokens": toks, "algorithmic_bytes": nbytes,
             "attn_us": round(t_split * 1e6, 2), "combine_us": round(t_comb * 1e6, 2),
             "attn_gbps": round(nbytes / t_split / 1e9, 1),
             "attn_frac": round(nbytes / t_split / 1e9 / HBM_PEAK_GBPS, 4),
-            "packed_tokens_per_s_attention": round(toks / (t_split + t_comb), 1)}
+            "op_us": round(t_op * 1e6, 2),
+            "op_gbps": round(nbytes / t_op / 1e9, 1),
+            "op_frac": round(nbytes / t_op / 1e9 / HBM_PEAK_GBPS, 4),
+            "us_per_layer": round(t_op * 1e6, 2),
+            "packed_tokens_per_s_attention": round(toks / t_op, 1),
+            "timing": "median of %d launches per kernel (timing-only HIP events)"
+                      % tm.count("attn_split")}
         del q, kv, o, scrub
         torch.cuda.empty_cache()
     return out
@@ -580,7 +618,7 @@ def main():
     log("step %.1f us, %.0f tokens/s" % (ms_step * 1e3, value))
 
     # ---- kernel durations: HIP events around each kernel on its stream
-    n_timed = max(args.steps, 20)
+    n_timed = max(args.steps, 200)
     for _ in range(3):
         step_on(stream)
     torch.cuda.synchronize()
@@ -589,10 +627,11 @@ def main():
         for _ in range(n_timed):
             step_on(stream)
         torch.cuda.synchronize()
-    t_split = timer.mean_ms("attn_split") * 1e-3
-    t_comb = timer.mean_ms("attn_combine") * 1e-3
-    t_argmax = timer.mean_ms("accept_argmax") * 1e-3
-    t_prefix = timer.mean_ms("accept_prefix") * 1e-3
+    t_split = timer.median_ms("attn_split") * 1e-3
+    t_comb = timer.median_ms("attn_combine") * 1e-3
+    t_argmax = timer.median_ms("accept_argmax") * 1e-3
+    t_prefix = timer.median_ms("accept_prefix") * 1e-3
+    t_split_mean = timer.mean_ms("attn_split") * 1e-3
 
     hq, hkv, d = attn.num_q_heads, attn.num_kv_heads, attn.head_dim
     b_attn = attention_bytes(attn, hkv, hq, d)
@@ -637,15 +676,37 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes": b_attn,
             "launch_us": round(t_split * 1e6, 2),
+            "launch_us_mean": round(t_split_mean * 1e6, 2),
             "timing": "timing-only HIP events (hipEventDisableSystemFence) around each "
-                      "launch on its stream, %d launches" % n_timed,
+                      "launch on its stream; median of %d launches" % timer.count("attn_split"),
+            # the same bytes over whole operations, not the dominant kernel alone
+            "attention_op_frac": round(b_attn / (t_split + t_comb) / 1e9 / HBM_PEAK_GBPS, 4),
+            "acceptance_op_frac": round(b_acc / (t_argmax + t_prefix) / 1e9 / HBM_PEAK_GBPS, 4),
+            "step_frac": round((b_attn + b_acc) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        },
+        "operations": {
+            "attention": {"kernels": "attn_streamk_kernel + attn_combine_kernel",
+                          "us": round((t_split + t_comb) * 1e6, 2),
+                          "algorithmic_bytes": b_attn,
+                          "gbps": round(b_attn / (t_split + t_comb) / 1e9, 1),
+                          "frac": round(b_attn / (t_split + t_comb) / 1e9 / HBM_PEAK_GBPS, 4)},
+            "acceptance": {"kernels": "argmax_chunk_kernel + prefix_kernel",
+                           "us": round((t_argmax + t_prefix) * 1e6, 2),
+                           "algorithmic_bytes": b_acc,
+                           "gbps": round(b_acc / (t_argmax + t_prefix) / 1e9, 1),
+                           "frac": round(b_acc / (t_argmax + t_prefix) / 1e9 / HBM_PEAK_GBPS, 4)},
+            "step": {"what": "one graph replay of all four kernels (ms_per_step)",
+                     "us": round(ms_step * 1e3, 2), "algorithmic_bytes": b_attn + b_acc,
+                     "gbps": round((b_attn + b_acc) / (ms_step * 1e-3) / 1e9, 1),
+                     "frac": round((b_attn + b_acc) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
         },
         "us_per_layer_attention": round((t_split + t_comb) * 1e6, 2),
         "attention_gbps": round(b_attn / (t_split + t_comb) / 1e9, 1),
         "attention_tflops": round(f_attn / (t_split + t_comb) / 1e12, 2),
         "accept": {"argmax_us": round(t_argmax * 1e6, 2), "prefix_us": round(t_prefix * 1e6, 2),
                    "algorithmic_bytes": b_acc, "argmax_gbps": round(a_gbps, 1),
-                   "argmax_frac": round(a_gbps / HBM_PEAK_GBPS, 4)},
+                   "argmax_frac": round(a_gbps / HBM_PEAK_GBPS, 4),
+                   "op_frac": round(b_acc / (t_argmax + t_prefix) / 1e9 / HBM_PEAK_GBPS, 4)},
         "combine_us": round(t_comb * 1e6, 2),
     }
     graph.close()
@@ -677,14 +738,15 @@ def main():
         for _ in range(n_timed):
             smp()
         torch.cuda.synchronize()
-    t_stats = timer.mean_ms("sample_stats") * 1e-3
-    t_draw = timer.mean_ms("sample_draw") * 1e-3
+    t_stats = timer.median_ms("sample_stats") * 1e-3
+    t_draw = timer.median_ms("sample_draw") * 1e-3
     s_gbps = b_acc / t_stats / 1e9
     result["stochastic_accept"] = {
         "temperature": 1.0, "stats_us": round(t_stats * 1e6, 2),
         "draw_us": round(t_draw * 1e6, 2), "algorithmic_bytes": b_acc,
         "stats_gbps": round(s_gbps, 1), "stats_frac": round(s_gbps / HBM_PEAK_GBPS, 4),
-        "timing": "timing-only HIP events around each launch, %d launches" % n_timed}
+        "timing": "timing-only HIP events around each launch, median of %d launches"
+                  % timer.count("sample_stats")}
 
     del q, kv, logits, out
     torch.cuda.empty_cache()

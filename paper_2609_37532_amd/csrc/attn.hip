@@ -1030,7 +1030,7 @@ int resident_workgroups(int head_dim) {
 }  // namespace
 
 // Upper bound of the persistent grid, known without a device: at most 1024
-// workgroups (a 256-CU MI355X holds 768 of this kernel at once) and never
+// workgroups (a 256-CU MI355X holds 512 of this kernel at once, two per CU) and never
 // more than the 32-key blocks the largest batch could hold.  The workspace
 // is sized for it.
 int32_t attn_grid_cap(const dsv_attn_dims &d) {

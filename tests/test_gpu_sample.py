@@ -3,8 +3,9 @@ through the C ABI.
 
 The result is a function of the caller's uniforms, so each request is
 compared exactly with the fp64 oracle unless one of its uniforms lies within
-1e-4 of the threshold it was compared with (the oracle reports that margin);
-such requests only have to be valid.  Independently of the oracle, a
+TOL = 1e-5 of the threshold it was compared with (the oracle reports that
+margin); such requests only have to be valid, and the successor must occupy
+a cumulative interval within TOL of its uniform.  Independently of the oracle, a
 chi-square test checks that the first token the GPU emits follows the target
 distribution of the anchor row (the verifier is lossless), and at very low
 temperature the result must equal the greedy verifier's.
