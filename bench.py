@@ -52,6 +52,11 @@ def parse():
     ap.add_argument("--eager-only", type=int, default=0, metavar="N",
                     help="only run N eager steps (no graph, no timing, no CPU "
                          "baseline): the program that hardware-counter passes profile")
+    ap.add_argument("--eager-attention", type=int, default=0, metavar="C",
+                    help="with --eager-only N: run N eager verify-attention launches of "
+                         "config C (2, 3 or 4), or of one layer of the 36-layer stress "
+                         "run at its first step (5), with a 512 MB scrub before each, and "
+                         "nothing else: the program that per-shape counter passes profile")
     ap.add_argument("--no-stress", action="store_true",
                     help="skip the 36-layer graph-replay stress measurement")
     ap.add_argument("--stress-steps", type=int, default=100)
@@ -300,7 +305,7 @@ def configs_bench(reps=200):
                 run()
             torch.cuda.synchronize()
         t_split = tm.median_ms("attn_split") * 1e-3
-        t_comb = tm.median_ms("attn_combine") * 1e-3
+        t_comb = tm.median_ms("attn_combine") * 1e-3 if tm.count("attn_combine") else 0.0
         nbytes = attention_bytes(attn, attn.num_kv_heads, attn.num_q_heads, attn.head_dim)
         toks = int(attn.qlens.sum())
         t_op = t_split + t_comb
@@ -538,6 +543,48 @@ def copy_probe():
     print(json.dumps({"copy_probe_bytes": n, "copies": 3}), flush=True)
 
 
+def eager_attention(cfg, launches):
+    """``launches`` eager verify-attention launches of one shape, each after a
+    512 MB scrub (so the KV comes from HBM), for hardware-counter passes.
+    cfg 2-4: the attention configs; 5: one layer of the stress run's first
+    step (B=32, contexts U[512, 4096], verify lengths of that step)."""
+    import torch
+
+    import paper_2609_37532_amd as dsv
+    import workloads as W
+    dev = "cuda"
+    if cfg == 5:
+        plan = W.StressPlan(steps=1)
+        st = plan.draw_step()
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(W.SEED_BASE + 5)
+        hq, hkv, d = 32, 8, 128
+        kv = torch.randn((plan.num_pages, 2, hkv, W.PAGE_SIZE * d), generator=gen, device=dev,
+                         dtype=torch.bfloat16)
+        q = torch.randn((plan.capacity, hq, d), generator=gen, device=dev, dtype=torch.bfloat16)
+        cu = torch.from_numpy(st.cu_qlens).to(dev)
+        ctx = torch.from_numpy(plan.ctx0.astype(np.int32)).to(dev)
+        pt = torch.from_numpy(plan.page_table).to(dev)
+        max_kv_len, scale = plan.max_kv_len, 1.0 / np.sqrt(d)
+    else:
+        a = W.config_attn_inputs(cfg)
+        bf = lambda x: torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(dev).view(
+            torch.bfloat16)
+        i32 = lambda x: torch.from_numpy(np.ascontiguousarray(x, dtype=np.int32)).to(dev)
+        q, kv = bf(a.q), bf(a.kv_pages)
+        cu, pt, ctx = i32(a.cu_qlens), i32(a.page_table), i32(a.ctx_lens)
+        max_kv_len, scale = a.max_kv_len, a.scale
+    out = torch.zeros_like(q)
+    dims = dsv.attn_dims(q, kv, pt, max_kv_len=max_kv_len, scale=scale)
+    ws = dsv.alloc_workspace(dsv.verify_attn_workspace_bytes(dims), dev)
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    for r in range(launches):
+        scrub.fill_(r & 0xFF)
+        dsv.verify_attn(q, cu, kv, pt, ctx, out, dims=dims, workspace=ws)
+    torch.cuda.synchronize()
+    print(json.dumps({"eager_attention_config": cfg, "launches": launches}), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -557,6 +604,9 @@ def main():
     import workloads as W
 
     dev = torch.device("cuda", 0)
+    if args.eager_only and args.eager_attention:
+        eager_attention(args.eager_attention, args.eager_only)
+        return
     t0 = time.time()
     rng = W.config_rng(CONFIG_INDEX)
     attn = W.config_attn_inputs(CONFIG_INDEX, rng=rng)
@@ -628,7 +678,7 @@ def main():
             step_on(stream)
         torch.cuda.synchronize()
     t_split = timer.median_ms("attn_split") * 1e-3
-    t_comb = timer.median_ms("attn_combine") * 1e-3
+    t_comb = timer.median_ms("attn_combine") * 1e-3 if timer.count("attn_combine") else 0.0
     t_argmax = timer.median_ms("accept_argmax") * 1e-3
     t_prefix = timer.median_ms("accept_prefix") * 1e-3
     t_split_mean = timer.mean_ms("attn_split") * 1e-3

@@ -145,7 +145,15 @@ size_t dsv_verify_attn_workspace_bytes(const dsv_attn_dims *dims);
  *                 K tile: element (slot s, dim d) at ((d/8)*16 + s)*8 + d%8
  *                         (8-element d-chunks, slot-major inside a chunk);
  *                 V tile: element (slot s, dim d) at d*16 + s (d-major).
- *               Each tile is 16*D*2 bytes (4 KiB at D=128).
+ *               Each tile is 16*D*2 bytes (4 KiB at D=128).  This is the
+ *               format every KV writer (the target's KV-cache append) must
+ *               produce; it is not the plain [16][D] row layout.  The V tile
+ *               must be d-major because the PV product contracts over keys:
+ *               one lane's operand is 8 consecutive keys of one dim, which
+ *               a plain tile would spread over 8 rows (transposing it at the
+ *               LDS store measured 26% slower at Qwen3-8B shape, B=32); the
+ *               K tile's 8-dim chunks measured within 1% of a plain K tile
+ *               there and up to 4% faster at smaller batches.
  *   page_table  int32 [B][P_max]; only the first ceil((ctx_i+k_i)/16) entries
  *               of row i are read.
  *   ctx_lens    int32 [B], committed context EXCLUDING the verify block, >= 0,
@@ -155,10 +163,11 @@ size_t dsv_verify_attn_workspace_bytes(const dsv_attn_dims *dims);
  *               aligned.
  * q_packed, kv_pages and out must be 16-byte aligned (every base allocation
  * is); DSV_ERR_UNSUPPORTED otherwise, with nothing enqueued.
- * Precision: q.k products, the softmax and all accumulation are fp32; the
- * softmax weights enter the weighted sum of V rounded to bf16 (and the same
- * rounded weights form the normaliser); `out` is rounded once to bf16
- * (round-to-nearest-even).  Results are bitwise deterministic for given
+ * Precision: q.k products, the softmax and all accumulation are fp32; each
+ * softmax weight enters the weighted sum of V as a pair of bf16 values (the
+ * weight rounded, then the remainder rounded), about 2^-17 of its value, and
+ * the normaliser is the fp32 sum of the weights; `out` is rounded once to
+ * bf16 (round-to-nearest-even).  Results are bitwise deterministic for given
  * inputs and do not depend on which physical pages hold the keys.  How the
  * other requests are packed changes a request's result only through the
  * summation order (the work split follows the batch's total work), i.e.
