@@ -46,6 +46,8 @@
 //    so rescales and merge weights are exact powers of two.
 //  * Waves of a workgroup split the dims when a request has one or two row
 //    tiles; with three or more row tiles each wave owns tiles.
+//  * The workgroup placed second on a CU runs at raised wave priority over
+//    most of its share, so that both workgroups of a CU finish together.
 #include "dsv_internal.h"
 
 #include <math.h>
@@ -67,6 +69,15 @@ constexpr int kMinShare = 8 * kBlockKeys;
 // shares are equal in streaming plus piece starts.  A multiple of the block;
 // six blocks measured best across shapes (two to eight were compared).
 constexpr int kLeadKeys = kAttnLeadKeys;
+// Wave priority.  The persistent grid holds two workgroups per CU, and the
+// one the dispatcher places second (grid index >= number of CUs) loses
+// instruction arbitration to the older first one: with equal shares it
+// finished several microseconds later, and the CU's last stretch ran on one
+// workgroup.  Its waves therefore run at raised priority until kBoostPct
+// percent of its share is done, then at the default.  Priority changes no
+// arithmetic.  Drop points of 50, 65, 80 and 90 percent and the whole share
+// were compared; 65 gained the most over shapes.
+constexpr int kBoostPct = 65;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
   return __builtin_bit_cast(bf16x8, v);
@@ -656,6 +667,7 @@ struct RingCtx {
   uint32_t vb;           // V operand offset of the wave's first d block
   int nblk;              // blocks in the sub-piece
   int sb, se, ctx, row_limit;
+  int prio_end_b;        // block at which the wave priority returns to the default
   bool active;
 };
 
@@ -681,6 +693,7 @@ __device__ __forceinline__ void ring_step(const RingCtx<D> &c, char *ring, int b
   stage_store<D>(ring + ST * R::kStage + c.dst0, lane, regs);
   stage_load<D>(tile_of<D>(c, b + kStages), c.voff, regs);
   __syncthreads();
+  if (b == c.prio_end_b) __builtin_amdgcn_s_setprio(0);
   if (c.active) {
     const int t0 = c.sb + b * kBlockKeys;
     const bool full = t0 + kBlockKeys <= min(c.ctx, c.se);
@@ -746,6 +759,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
   const int kq = lane >> 4, n = lane & 15;
+  // keys of the share (virtual) run at raised priority; -1: none
+  const bool boost = (int)blockIdx.x >= p.num_cu;
+  if (boost) __builtin_amdgcn_s_setprio(1);
+  const int boost_keys = boost ? (int)((long long)(sh.end - sh.start) * kBoostPct / 100) : -1;
 
   // this wave's share of every ring load: page parity pp, K (waves 0-1) or V
   const int pp = wave & 1, kind = wave >> 1;
@@ -829,6 +846,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
         c.sb = sb;
         c.se = se;
         c.nblk = (se - sb + kBlockKeys - 1) / kBlockKeys;
+        c.prio_end_b = -1;
+        if (boost_keys >= 0) {
+          const int left = boost_keys - ((pos - sh.start) + (sb - key_begin));
+          c.prio_end_b = left <= 0 ? 0 : (left + kBlockKeys - 1) / kBlockKeys;
+        }
         // stage the sub-piece's page ids; an id outside [0, num_pages) breaks
         // the contract and reads page 0 instead (valid memory, result
         // unspecified), pages past the sub-piece read page 0 and are masked
