@@ -57,6 +57,10 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
+// Combine kernel: 1024-thread workgroups (32 rows at D = 128) need a quarter
+// of the workgroups that 256 threads do, most of which exit at once; measured
+// 0.6 us faster at config 4 and 0.5% on the 36-layer step.
+constexpr int kCombThreads = 1024;
 constexpr int kBlockKeys = kAttnBlockKeys;  // keys per inner step (two pages)
 // Smallest stream-K share: with little work (short contexts, few requests)
 // eight blocks per workgroup beat spreading it over every resident
@@ -888,21 +892,21 @@ __global__ __launch_bounds__(kThreads, 2) void attn_streamk_kernel(AttnParams p)
 
 // Merges the partials of segments that straddle share boundaries (in
 // workgroup order, so the result is deterministic) and zeroes the tail rows.
-// Workgroup (x, g, i) owns 256/(D/4) live rows of request i and KV head g;
+// Workgroup (x, g, i) owns kCombThreads/(D/4) live rows of request i and KV head g;
 // each thread owns 4 output dims of one row and issues the loads of up to 8
 // partials at a time.  Workgroups with z == B zero the tail rows instead.
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_combine_kernel(AttnParams p) {
+__global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnParams p) {
   constexpr int kLanesPerRow = D / 4;
-  constexpr int kRows = kThreads / kLanesPerRow;
+  constexpr int kRows = kCombThreads / kLanesPerRow;
   const int g = blockIdx.y, i = blockIdx.z;
   const int G = p.group;
   if (i == p.num_reqs) {
     const int live = min(max(p.cu[p.num_reqs], 0), p.cap);
     const int per_row = G * (D / 8);
     const int total = (p.cap - live) * per_row;
-    for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < total;
-         idx += gridDim.x * kThreads) {
+    for (int idx = blockIdx.x * kCombThreads + threadIdx.x; idx < total;
+         idx += gridDim.x * kCombThreads) {
       const int r = live + idx / per_row, rem = idx % per_row;
       const int hh = rem / (D / 8), d8 = rem % (D / 8);
       uint16_t *o = p.out + ((size_t)r * p.hq + (size_t)g * G + hh) * D + 8 * d8;
@@ -1086,7 +1090,7 @@ AttnWorkspace attn_workspace_layout(const dsv_attn_dims &d) {
 
 hipError_t launch_verify_attn(const AttnParams &p, int head_dim, hipStream_t s) {
   // rows of one request and KV head: G * k_i <= G * 16
-  const int comb_rows = head_dim == 128 ? kThreads / 32 : kThreads / 16;
+  const int comb_rows = head_dim == 128 ? kCombThreads / 32 : kCombThreads / 16;
   const dim3 grid_comb((p.group * kMaxQlen + comb_rows - 1) / comb_rows, p.hkv,
                        p.num_reqs + 1);
   timing_mark(kTimeAttnSplit, false, s);
@@ -1097,9 +1101,9 @@ hipError_t launch_verify_attn(const AttnParams &p, int head_dim, hipStream_t s) 
   timing_mark(kTimeAttnSplit, true, s);
   timing_mark(kTimeAttnCombine, false, s);
   if (head_dim == 128)
-    hipLaunchKernelGGL(attn_combine_kernel<128>, grid_comb, dim3(kThreads), 0, s, p);
+    hipLaunchKernelGGL(attn_combine_kernel<128>, grid_comb, dim3(kCombThreads), 0, s, p);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<64>, grid_comb, dim3(kThreads), 0, s, p);
+    hipLaunchKernelGGL(attn_combine_kernel<64>, grid_comb, dim3(kCombThreads), 0, s, p);
   timing_mark(kTimeAttnCombine, true, s);
   return hipGetLastError();
 }
