@@ -16,8 +16,9 @@
 //    ceil32(ctx_i + k_i) keys; the segments are laid end to end, each
 //    after a lead-in of six blocks that stands for the cost of starting a
 //    piece on it, and a persistent grid, sized to the workgroups the GPU
-//    holds at once, gives every workgroup one equal contiguous share of
-//    that space (streaming plus piece starts).  A workgroup walks the
+//    holds at once, gives every workgroup one contiguous share of that
+//    space (streaming plus piece starts), equal up to a small skew by grid
+//    index parity for the XCDs' unequal streaming rates.  A workgroup walks the
 //    segments its share touches; a segment it covers whole is written as
 //    bf16 directly, a segment cut at a share boundary leaves an fp32 partial
 //    (O, m, l) that the combine kernel merges in workgroup order.  Ragged
@@ -433,6 +434,27 @@ __device__ __forceinline__ int piece_begin(int seg, int n, int q) {
   return (int)((long long)(seg / kBlockKeys) * q / n) * kBlockKeys;
 }
 
+// Stream-K shares alternate in size with the workgroup's grid index.  The
+// dispatcher places workgroup b on XCD b mod 8, and with equal shares the
+// workgroups on the odd XCDs finished 6-10 us after those on the even ones
+// in every clocked launch of the Qwen3-8B shape at B=32, contexts up to 8K,
+// while the shader clocks of all eight XCDs agreed within 2%.  Even
+// workgroups therefore take kSkewPct percent more than the mean share and
+// odd ones as much less (whole blocks).
+constexpr int kSkewPct = 6;
+__device__ __forceinline__ int share_skew(int share) {
+  return (int)((long long)share * kSkewPct / 100) / kBlockKeys * kBlockKeys;
+}
+// First virtual key of workgroup b's share.
+__device__ __forceinline__ int share_begin(int b, int share, int skew) {
+  return b * share + (b & 1) * skew;
+}
+// The workgroup whose share holds virtual key pos.
+__device__ __forceinline__ int share_owner(int pos, int share, int skew) {
+  const int pair = pos / (2 * share);
+  return 2 * pair + (pos - pair * 2 * share >= share + skew ? 1 : 0);
+}
+
 // Inclusive prefix sum over the 64 lanes of a wave with DPP row shifts and
 // row broadcasts (lanes without a source add 0): six VALU steps, where a
 // shuffle-based scan would take six LDS permutes.
@@ -579,8 +601,9 @@ __device__ Share plan_share(const AttnParams &p, int *lds) {
   const int b = (int)blockIdx.x;
   int start = work_s, end = work_s;
   if (!seg_mode) {
-    start = min(work_s, b * share);
-    end = min(work_s, start + share);
+    const int skew = share_skew(share);
+    start = min(work_s, share_begin(b, share, skew));
+    end = min(work_s, share_begin(b + 1, share, skew));
   }
   // the thread whose requests contain this workgroup's share locates it and
   // publishes the request's metadata, so the first piece needs no second
@@ -933,6 +956,7 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnParams p
   const int seg = next - prefix;
   if (seg <= 0) return;
   const int start = prefix * p.hkv + g * seg;
+  const int skew = share > 0 ? share_skew(share) : 0;
   int b0, b1;
   if (share <= 0) {
     // small-batch plan: the segment's n pieces sit on consecutive workgroups,
@@ -943,8 +967,8 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnParams p
   } else {
     // stream-K: seg includes the lead-in, and the first workgroup with any
     // of the segment's keys is the one holding the first key after it
-    b0 = (start + kLeadKeys) / share;
-    b1 = (start + seg - 1) / share;
+    b0 = share_owner(start + kLeadKeys, share, skew);
+    b1 = share_owner(start + seg - 1, share, skew);
   }
   if (b0 == b1) return;  // one workgroup held the whole segment
   const int rr = blockIdx.x * kRows + threadIdx.x / kLanesPerRow;
@@ -958,7 +982,7 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(AttnParams p
   // segment, else slot 1 (the segment is where its share ends)
   auto prow = [&](int u) -> size_t {
     const int b = b0 + u;
-    const int slot = share <= 0 || b * share >= start ? 0 : 1;
+    const int slot = share <= 0 || share_begin(b, share, skew) >= start ? 0 : 1;
     return ((size_t)b * 2 + slot) * (G * kMaxQlen) + rr;
   };
 

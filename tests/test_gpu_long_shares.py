@@ -29,23 +29,40 @@ except Exception:  # pragma: no cover
 
 STAGE_KEYS = 512 * W.PAGE_SIZE  # keys whose page ids the kernel stages at a time
 LEAD = 6 * 32                   # stream-K lead-in of virtual keys per segment
+SKEW_PCT = 6                    # even workgroups' shares are this much larger, odd ones' smaller
+
+
+def share_bounds(b, share):
+    """[begin, end) of workgroup b's share in the virtual space, as the kernel
+    lays them out: pairs of shares of share +- skew (whole 32-key blocks)."""
+    skew = share * SKEW_PCT // 100 // 32 * 32
+    begin = lambda w: w * share + (w & 1) * skew
+    return begin(b), begin(b + 1)
 
 
 def pieces_of(plan, B, hkv, seg_keys):
     """Key length of every (request, KV head, workgroup) piece, from the plan
     the kernel published: plan[i] = virtual prefix of request i, plan[B+1] =
-    share.  Segment (i, g) occupies [plan[i]*hkv + g*segv, + segv) of the
-    virtual space, its keys after a lead-in of LEAD."""
+    mean share.  Segment (i, g) occupies [plan[i]*hkv + g*segv, + segv) of
+    the virtual space, its keys after a lead-in of LEAD."""
     share = int(plan[B + 1])
+    total = int(plan[B]) * hkv
+    bounds = []
+    b = 0
+    while True:
+        lo, hi = share_bounds(b, share)
+        if lo >= total:
+            break
+        bounds.append((lo, min(hi, total)))
+        b += 1
     out = {}
     for i in range(B):
         segv = seg_keys[i] + LEAD
         for g in range(hkv):
             s0 = int(plan[i]) * hkv + g * segv
             k0, k1 = s0 + LEAD, s0 + segv
-            b0, b1 = k0 // share, (k1 - 1) // share
-            out[(i, g)] = [min(k1, (b + 1) * share) - max(k0, b * share)
-                           for b in range(b0, b1 + 1)]
+            out[(i, g)] = [min(k1, hi) - max(k0, lo) for lo, hi in bounds
+                           if min(k1, hi) > max(k0, lo)]
     return share, out
 
 
